@@ -1,0 +1,242 @@
+"""CPU oracle for BAPS attention -- TEST INFRASTRUCTURE ONLY.
+
+A plain, slow, fp64 implementation of what the BAPS path computes, written
+from the paper (arXiv 2602.02071): eq. (1) attention, eq. (2) base-2 online
+softmax, eq. (3) offloaded subtraction, Sec. 3.3 integer powers of two,
+Alg. 1 (the proposed workflow) and Alg. 2 (App. A, exp2 in HiF8), plus the
+HiF8 format the paper cites.  The arithmetic lives in ``baps_oracle.c``
+(plain C, compiled with gcc); this module only marshals numpy arrays.
+
+Only the test suite, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  It shares no code with the HIP
+library in ``paper_2602_02071_amd``, and that library never imports it.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liborc.so")
+SOURCE = os.path.join(_HERE, "baps_oracle.c")
+
+# attention setups (Sec. 4.1 and Table 1 of the paper)
+E2E_HIF8 = 0        # Alg. 1, the "E2E HiF8" setup (the canonical BAPS result)
+DEFAULT = 1         # eq. (2) with an fp32 softmax ("Default")
+EXP2_HIF8 = 2       # eq. (2) with every power of two in HiF8 ("Exp2 HiF8")
+NAIVE_E2E = 3       # scores cast to HiF8 before the max subtraction ("Naive E2E")
+EXP2_E4M3 = 4
+EXP2_E5M2 = 5
+EXP2_E4M3xE5M2 = 6
+E2E_EXACT = 7       # Alg. 1 control flow with the 8-bit casts removed, fp64 arithmetic
+
+_lib = None
+
+
+def build(force: bool = False) -> str:
+    """Compile the oracle with gcc (no contraction, no fast-math)."""
+    if force or not os.path.exists(LIB_PATH) or os.path.getmtime(LIB_PATH) < os.path.getmtime(SOURCE):
+        tmp = LIB_PATH + ".tmp%d" % os.getpid()
+        subprocess.check_call([
+            "gcc", "-O2", "-std=gnu11", "-fPIC", "-shared", "-ffp-contract=off",
+            "-fno-fast-math", "-Wall", "-o", tmp, SOURCE, "-lm", "-lpthread"])
+        os.replace(tmp, LIB_PATH)
+    return LIB_PATH
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    build()
+    L = ctypes.CDLL(LIB_PATH)
+    P = ctypes.c_void_p
+    i64 = ctypes.c_int64
+    i32 = ctypes.c_int
+    d = ctypes.c_double
+    L.orc_hif8_decode.restype = d
+    L.orc_hif8_decode.argtypes = [i32]
+    L.orc_hif8_encode.restype = i32
+    L.orc_hif8_encode.argtypes = [d, i32]
+    L.orc_hif8_round.restype = d
+    L.orc_hif8_round.argtypes = [d, i32]
+    L.orc_e4m3_encode.restype = i32
+    L.orc_e4m3_encode.argtypes = [d]
+    L.orc_e5m2_encode.restype = i32
+    L.orc_e5m2_encode.argtypes = [d]
+    L.orc_e4m3_decode.restype = d
+    L.orc_e4m3_decode.argtypes = [i32]
+    L.orc_e5m2_decode.restype = d
+    L.orc_e5m2_decode.argtypes = [i32]
+    L.orc_round_fp16.restype = d
+    L.orc_round_fp16.argtypes = [d]
+    L.orc_default_threads.restype = i32
+    L.orc_default_threads.argtypes = []
+    L.orc_hif8_encode_f32.restype = None
+    L.orc_hif8_encode_f32.argtypes = [P, P, i64, i32, i32]
+    L.orc_hif8_check_patterns.restype = i64
+    L.orc_hif8_check_patterns.argtypes = [ctypes.c_uint64, i64, P, i32, i32, ctypes.POINTER(i64)]
+    L.orc_exp2_table.restype = None
+    L.orc_exp2_table.argtypes = [P, i32]
+    L.orc_attention.restype = i32
+    L.orc_attention.argtypes = [P, P, P, i32, i32, i32, i32, i32, i32, i32, i32,
+                                i32, i32, i32, i32, d, P, i64, P, P, P, i32]
+    L.orc_exact_attention.restype = i32
+    L.orc_exact_attention.argtypes = [P, P, P, i32, i32, i32, i32, i32, i32, i32,
+                                      d, P, i64, P, P, i32]
+    L.orc_softmax_block.restype = i32
+    L.orc_softmax_block.argtypes = [P, i64, i64, i64, i32, i32, i32, P, P, P, P, P, i32]
+    _lib = L
+    return L
+
+
+def _ptr(a: np.ndarray):
+    return ctypes.c_void_p(a.ctypes.data) if a is not None else None
+
+
+def default_threads() -> int:
+    return int(_load().orc_default_threads())
+
+
+# ---------------------------------------------------------------- HiF8 codec
+def hif8_decode(codes) -> np.ndarray:
+    """Value of each HiF8 code (NaN / +-Inf for the special codes)."""
+    L = _load()
+    codes = np.asarray(codes, dtype=np.int64)
+    table = np.array([L.orc_hif8_decode(c) for c in range(256)], dtype=np.float64)
+    return table[codes]
+
+
+def hif8_encode(x, saturate: bool = True, nthreads: int = 0) -> np.ndarray:
+    """Round-to-nearest (ties away) HiF8 code of each fp32 value."""
+    L = _load()
+    x = np.ascontiguousarray(np.asarray(x, dtype=np.float32))
+    out = np.empty(x.shape, dtype=np.uint8)
+    L.orc_hif8_encode_f32(_ptr(x), _ptr(out), x.size, int(saturate), nthreads)
+    return out
+
+
+def hif8_encode_scalar(x: float, saturate: bool = True) -> int:
+    return int(_load().orc_hif8_encode(float(x), int(saturate)))
+
+
+def hif8_round(x, saturate: bool = True) -> np.ndarray:
+    """The value each fp32 input takes after the 8-bit cast."""
+    return hif8_decode(hif8_encode(x, saturate))
+
+
+def check_patterns(start: int, codes: np.ndarray, saturate: bool = True, nthreads: int = 0):
+    """Compare codes[i] with the oracle's code for fp32 bit pattern start+i.
+    Returns (mismatch count, first mismatching index or -1)."""
+    L = _load()
+    codes = np.ascontiguousarray(codes, dtype=np.uint8)
+    first = ctypes.c_int64(-1)
+    bad = L.orc_hif8_check_patterns(ctypes.c_uint64(start), codes.size, _ptr(codes),
+                                    int(saturate), nthreads, ctypes.byref(first))
+    return int(bad), int(first.value)
+
+
+def exp2_table(variant: int = 0) -> np.ndarray:
+    """code -> code of HiF8(2^x).  variant 0: fp64 exp2, one rounding;
+    variant 1: Alg. 2 with its FP16 carrier."""
+    out = np.zeros(256, dtype=np.uint8)
+    _load().orc_exp2_table(_ptr(out), int(variant))
+    return out
+
+
+def round_fp16(y: float) -> float:
+    return float(_load().orc_round_fp16(float(y)))
+
+
+def e4m3_encode(x: float) -> int:
+    return int(_load().orc_e4m3_encode(float(x)))
+
+
+def e5m2_encode(x: float) -> int:
+    return int(_load().orc_e5m2_encode(float(x)))
+
+
+def e4m3_decode(c: int) -> float:
+    return float(_load().orc_e4m3_decode(int(c)))
+
+
+def e5m2_decode(c: int) -> float:
+    return float(_load().orc_e5m2_decode(int(c)))
+
+
+# ---------------------------------------------------------------- attention
+def _bits(a) -> np.ndarray:
+    a = np.ascontiguousarray(a)
+    if a.dtype != np.uint16:
+        raise TypeError("q/k/v must be bf16 bit patterns (np.uint16)")
+    return a
+
+
+def _rows(rows, total):
+    if rows is None:
+        return np.arange(total, dtype=np.int64)
+    rows = np.ascontiguousarray(np.asarray(rows, dtype=np.int64))
+    if rows.size and (rows.min() < 0 or rows.max() >= total):
+        raise ValueError("row index out of range")
+    return rows
+
+
+def attention(q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, block, mode=E2E_HIF8, lam=1, n_b0=1,
+              literal_else=False, scale_log2=0.0, rows=None, nthreads=0):
+    """Attention rows in one of the paper's setups.
+
+    q: [B,Hq,Sq,D], k/v: [B,Hkv,Sk,D] bf16 bit patterns.  rows: global row
+    indices (b*Hq + h)*Sq + r (all rows when None).  Returns (o[n,D] fp64,
+    lse[n] fp64, restarts[n] int32 -- restarted B1 blocks per row)."""
+    L = _load()
+    q, k, v = _bits(q), _bits(k), _bits(v)
+    rows = _rows(rows, B * Hq * Sq)
+    n = rows.size
+    o = np.zeros((n, D), dtype=np.float64)
+    lse = np.zeros(n, dtype=np.float64)
+    nrs = np.zeros(n, dtype=np.int32)
+    st = L.orc_attention(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, Sq, Sk, D, int(causal), block,
+                         int(mode), int(lam), int(n_b0), int(literal_else), float(scale_log2),
+                         _ptr(rows), n, _ptr(o), _ptr(lse), _ptr(nrs), int(nthreads))
+    if st:
+        raise ValueError("oracle rejected the attention arguments")
+    return o, lse, nrs
+
+
+def exact_attention(q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, scale_log2=0.0, rows=None, nthreads=0):
+    """eq. (1) in fp64.  Returns (o[n,D], lse[n])."""
+    L = _load()
+    q, k, v = _bits(q), _bits(k), _bits(v)
+    rows = _rows(rows, B * Hq * Sq)
+    n = rows.size
+    o = np.zeros((n, D), dtype=np.float64)
+    lse = np.zeros(n, dtype=np.float64)
+    st = L.orc_exact_attention(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, Sq, Sk, D, int(causal),
+                               float(scale_log2), _ptr(rows), n, _ptr(o), _ptr(lse), int(nthreads))
+    if st:
+        raise ValueError("oracle rejected the attention arguments")
+    return o, lse
+
+
+def softmax_block(s, block, lam=1, n_b0=1, nthreads=0):
+    """The vector-side steps of Alg. 1 on fp32 scores s[rows, cols] (log2
+    units, -inf = masked).  Returns codes[rows,cols] (uint8), ref_shift
+    [rows,nblk] (int32), m_final[rows], d_final[rows] (fp64), restarted
+    [rows,nblk] (uint8)."""
+    L = _load()
+    s = np.ascontiguousarray(np.asarray(s, dtype=np.float32))
+    rows, cols = s.shape
+    nblk = (cols + block - 1) // block
+    codes = np.zeros((rows, cols), dtype=np.uint8)
+    refs = np.zeros((rows, nblk), dtype=np.int32)
+    m = np.zeros(rows, dtype=np.float64)
+    d = np.zeros(rows, dtype=np.float64)
+    rs = np.zeros((rows, nblk), dtype=np.uint8)
+    st = L.orc_softmax_block(_ptr(s), rows, cols, cols, block, int(lam), int(n_b0), _ptr(codes),
+                             _ptr(refs), _ptr(m), _ptr(d), _ptr(rs), int(nthreads))
+    if st:
+        raise ValueError("oracle rejected the softmax-block arguments")
+    return codes, refs, m, d, rs

@@ -1,0 +1,716 @@
+/*
+ * BAPS CPU oracle.  TEST INFRASTRUCTURE ONLY.
+ *
+ * A plain, slow, obviously-correct CPU implementation of what the BAPS
+ * attention path computes, written from the paper "BAPS: A Fine-Grained
+ * Low-Precision Scheme for Softmax in Attention via Block-Aware Precision
+ * reScaling" (arXiv 2602.02071):
+ *   - eq. (1)   standard attention (the fp64 exact reference),
+ *   - eq. (2)   FlashAttention online softmax in base 2 (the "Default",
+ *               "Exp2 HiF8", "Naive E2E" and "Exp2 FP8" setups of Sec. 4.1
+ *               and Table 1),
+ *   - eq. (3)   the offloaded subtraction T = S - rowfill(m~) (Sec. 3.2),
+ *   - Sec. 3.3  integer powers of two for the rescale factors,
+ *   - Alg. 1    the proposed workflow ("E2E HiF8", Sec. 4.1),
+ *   - Alg. 2    (App. A) powers of two in HiF8, simulated through FP16,
+ * plus the HiF8 number format the paper cites (Luo et al. 2024, "Ascend
+ * HiFloat8 Format for Deep Learning"), decoded from its field layout.
+ *
+ * Floating point is fp64 unless the paper fixes the precision.  Nothing here
+ * is blocked, fused or reordered beyond what those definitions state.  Only
+ * the test suite, the smoke check and the benchmark's CPU-baseline leg load
+ * this library; it shares no code, header or table with the HIP library.
+ *
+ * Readings taken where the paper is silent or inconsistent (each one is also
+ * listed with its reason in the design notes of the repository):
+ *   R1  HiF8 code layout: sign | dot (11,10,01,001,0001,0000) | sign-magnitude
+ *       exponent with implicit leading one | mantissa; Inf = 0x6F/0xEF,
+ *       NaN = 0x80, zero = 0x00.
+ *   R2  rounding to nearest, ties away from zero, straight from the input
+ *       value (one rounding, no FP16 intermediate).
+ *   R3  finite overflow saturates to +-2^15; +-Inf stays +-Inf.
+ *   R5  the 8-bit exp2 is E8(t) = HiF8(exp2(t)) with exp2 in fp64.
+ *   R6  the integer row maximum uses ceil (Alg. 1).
+ *   R7  the else-branch of Alg. 1 scales the new block by 2^(m~ - m) as well
+ *       (the literal text leaves it unscaled; selectable for comparison).
+ *   R8  the restart decision is taken per query row.
+ *   R9  a B0 block is a forced restart: T = S - m and P = E8(HiF8(T)).
+ *   R10 B0 = the first n_b0 key blocks (n_b0 = 1), blocks visited in order.
+ *   R11 causal masks are bottom-right aligned: query r sees keys
+ *       c <= r + Sk - Sq; masked scores are -inf and drop out.
+ *   R13 lse = ln2 * (m + log2 d), natural log of the softmax denominator.
+ *   R15 S = fl32(acc * c) with acc = fl32(q.k) (dot product in fp64, rounded
+ *       once) and c = fl32(log2(e)/sqrt(d)); in the fused pass the product
+ *       and the subtraction of eq. (3) are one operation rounded once:
+ *       T = fl32(acc * c - ref).
+ *   R17 query head h reads key/value head h / (Hq/Hkv).
+ */
+#define _GNU_SOURCE
+#include <math.h>
+#include <pthread.h>
+#include <sched.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#include <unistd.h>
+
+/* ------------------------------------------------------------------------ */
+/* Number formats as value sets                                              */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+    int    n;              /* number of non-negative finite values, 0 included */
+    double val[256];       /* ascending */
+    int    code[256];      /* code of val[i] with a positive sign            */
+    int    neg_bit;        /* OR-ed into a code to make it negative          */
+    int    inf_code;       /* code of +Inf, -1 if the format has none        */
+    int    nan_code;       /* canonical NaN code                             */
+    double over_next;      /* nominal value after the maximum: a value rounds
+                              to +Inf (non-saturating) when it is at least the
+                              midpoint between the maximum and this value    */
+} orc_format;
+
+/* HiF8 decoding from the field layout (R1).  Returns the value of a code;
+ * NaN for the NaN code, +-Inf for the infinity codes. */
+double orc_hif8_decode(int code)
+{
+    int s = (code >> 7) & 1;
+    int b = code & 0x7f;
+    int es = 0, mag = 0, w, man, d_width;
+    if ((b >> 5) == 3) {            /* dot 11: D = 4, exponents +-8..+-15, 1 mantissa bit */
+        d_width = 4; es = (b >> 4) & 1; mag = 8 | ((b >> 1) & 7); w = 1; man = b & 1;
+    } else if ((b >> 5) == 2) {     /* dot 10: D = 3, exponents +-4..+-7, 2 mantissa bits */
+        d_width = 3; es = (b >> 4) & 1; mag = 4 | ((b >> 2) & 3); w = 2; man = b & 3;
+    } else if ((b >> 5) == 1) {     /* dot 01: D = 2, exponents +-2, +-3, 3 mantissa bits */
+        d_width = 2; es = (b >> 4) & 1; mag = 2 | ((b >> 3) & 1); w = 3; man = b & 7;
+    } else if ((b >> 4) == 1) {     /* dot 001: D = 1, exponents +-1, 3 mantissa bits */
+        d_width = 1; es = (b >> 3) & 1; mag = 1; w = 3; man = b & 7;
+    } else if ((b >> 3) == 1) {     /* dot 0001: D = 0, exponent 0, 3 mantissa bits */
+        d_width = 0; mag = 0; w = 3; man = b & 7;
+    } else {                        /* dot 0000: zero, NaN and the denormals 2^(M-23) */
+        man = b & 7;
+        if (man == 0) return s ? NAN : 0.0;
+        return (s ? -1.0 : 1.0) * ldexp(1.0, man - 23);
+    }
+    int e = es ? -mag : mag;
+    if (d_width == 4 && e == 15 && man == 1) return s ? -INFINITY : INFINITY;
+    return (s ? -1.0 : 1.0) * ldexp(1.0 + (double)man / (double)(1 << w), e);
+}
+
+/* OCP FP8 E4M3 (no infinities, max 448) and E5M2 (IEEE-like, max 57344),
+ * used only by the "Exp2 E4M3/E5M2/E4M3xE5M2" setups of Table 1. */
+static double e4m3_decode(int code)
+{
+    int s = (code >> 7) & 1, e = (code >> 3) & 15, m = code & 7;
+    double v;
+    if (e == 15 && m == 7) return NAN;
+    if (e == 0) v = ldexp((double)m, -9);
+    else v = ldexp(1.0 + m / 8.0, e - 7);
+    return s ? -v : v;
+}
+
+static double e5m2_decode(int code)
+{
+    int s = (code >> 7) & 1, e = (code >> 2) & 31, m = code & 3;
+    double v;
+    if (e == 31) return m ? NAN : (s ? -INFINITY : INFINITY);
+    if (e == 0) v = ldexp((double)m, -16);
+    else v = ldexp(1.0 + m / 4.0, e - 15);
+    return s ? -v : v;
+}
+
+static orc_format F_HIF8, F_E4M3, F_E5M2;
+
+static void build_format(orc_format* f, double (*dec)(int), int inf_code, int nan_code,
+                         double over_next)
+{
+    int n = 0;
+    for (int c = 0; c < 128; ++c) {
+        double v = dec(c);
+        if (!isfinite(v)) continue;
+        /* insertion sort keeps the table ascending */
+        int i = n++;
+        while (i > 0 && f->val[i - 1] > v) { f->val[i] = f->val[i - 1]; f->code[i] = f->code[i - 1]; --i; }
+        f->val[i] = v; f->code[i] = c;
+    }
+    f->n = n; f->neg_bit = 0x80; f->inf_code = inf_code; f->nan_code = nan_code;
+    f->over_next = over_next;
+}
+
+__attribute__((constructor)) static void init_formats(void)
+{
+    build_format(&F_HIF8, orc_hif8_decode, 0x6f, 0x80, 1.5 * 32768.0);
+    build_format(&F_E4M3, e4m3_decode, -1, 0x7f, 480.0);
+    build_format(&F_E5M2, e5m2_decode, 0x7c, 0x7f, 65536.0);
+}
+
+/* Round-to-nearest by search over the value set (R2: ties away from zero).
+ * Returns the index of the chosen non-negative value in f->val, or -1 for
+ * +Inf.  'a' is a non-negative magnitude (may be +Inf). */
+static int nearest_index(const orc_format* f, double a, int saturate)
+{
+    int top = f->n - 1;
+    if (isinf(a)) return f->inf_code >= 0 ? -1 : top;
+    if (a >= f->val[top]) {
+        if (saturate || f->inf_code < 0) return top;
+        return a >= 0.5 * (f->val[top] + f->over_next) ? -1 : top;
+    }
+    /* largest i with val[i] <= a */
+    int lo = 0, hi = top;
+    while (hi - lo > 1) {
+        int mid = (lo + hi) / 2;
+        if (f->val[mid] <= a) lo = mid; else hi = mid;
+    }
+    double midpoint = 0.5 * (f->val[lo] + f->val[lo + 1]);   /* exact in fp64 */
+    return a >= midpoint ? lo + 1 : lo;
+}
+
+static int fmt_encode(const orc_format* f, double x, int saturate)
+{
+    if (isnan(x)) return f->nan_code;
+    int i = nearest_index(f, fabs(x), saturate);
+    int code = i < 0 ? f->inf_code : f->code[i];
+    if (code == 0) return 0;                       /* -0 has no code of its own */
+    return signbit(x) ? (code | f->neg_bit) : code;
+}
+
+/* the value x rounds to (the 8-bit cast, "in 8-bit" of Alg. 1) */
+static double fmt_round(const orc_format* f, double x, int saturate)
+{
+    if (isnan(x)) return x;
+    int i = nearest_index(f, fabs(x), saturate);
+    double a = i < 0 ? INFINITY : f->val[i];
+    return signbit(x) ? -a : a;
+}
+
+int orc_hif8_encode(double x, int saturate) { return fmt_encode(&F_HIF8, x, saturate); }
+double orc_hif8_round(double x, int saturate) { return fmt_round(&F_HIF8, x, saturate); }
+int orc_e4m3_encode(double x) { return fmt_encode(&F_E4M3, x, 1); }
+int orc_e5m2_encode(double x) { return fmt_encode(&F_E5M2, x, 1); }
+double orc_e4m3_decode(int c) { return e4m3_decode(c); }
+double orc_e5m2_decode(int c) { return e5m2_decode(c); }
+
+/* ------------------------------------------------------------------------ */
+/* Threads                                                                   */
+/* ------------------------------------------------------------------------ */
+
+typedef void (*range_fn)(void* ctx, int64_t i0, int64_t i1);
+
+typedef struct {
+    range_fn fn; void* ctx; int64_t n, chunk; int64_t next;
+} pool_job;
+
+static void* pool_worker(void* arg)
+{
+    pool_job* j = (pool_job*)arg;
+    for (;;) {
+        int64_t i0 = __atomic_fetch_add(&j->next, j->chunk, __ATOMIC_RELAXED);
+        if (i0 >= j->n) break;
+        int64_t i1 = i0 + j->chunk < j->n ? i0 + j->chunk : j->n;
+        j->fn(j->ctx, i0, i1);
+    }
+    return NULL;
+}
+
+int orc_default_threads(void)
+{
+    cpu_set_t set;
+    if (sched_getaffinity(0, sizeof(set), &set) == 0) return CPU_COUNT(&set);
+    long n = sysconf(_SC_NPROCESSORS_ONLN);
+    return n > 0 ? (int)n : 1;
+}
+
+static void parallel_for(int64_t n, int nthreads, int64_t chunk, range_fn fn, void* ctx)
+{
+    if (n <= 0) return;
+    if (nthreads <= 0) nthreads = orc_default_threads();
+    if (nthreads > 256) nthreads = 256;
+    if (chunk <= 0) chunk = 1;
+    pool_job job = { fn, ctx, n, chunk, 0 };
+    if (nthreads == 1 || n <= chunk) { fn(ctx, 0, n); return; }
+    pthread_t th[256];
+    int started = 0;
+    for (int t = 0; t < nthreads; ++t)
+        if (pthread_create(&th[t], NULL, pool_worker, &job) == 0) ++started;
+    if (started == 0) { fn(ctx, 0, n); return; }
+    for (int t = 0; t < started; ++t) pthread_join(th[t], NULL);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Bulk encode and the exhaustive check helper                               */
+/* ------------------------------------------------------------------------ */
+
+typedef struct { const float* x; uint8_t* out; int sat; } enc_ctx;
+
+static void enc_range(void* p, int64_t i0, int64_t i1)
+{
+    enc_ctx* c = (enc_ctx*)p;
+    for (int64_t i = i0; i < i1; ++i) c->out[i] = (uint8_t)fmt_encode(&F_HIF8, (double)c->x[i], c->sat);
+}
+
+void orc_hif8_encode_f32(const float* x, uint8_t* out, int64_t n, int saturate, int nthreads)
+{
+    enc_ctx c = { x, out, saturate };
+    parallel_for(n, nthreads, 1 << 16, enc_range, &c);
+}
+
+typedef struct { uint64_t start; const uint8_t* got; int sat; int64_t bad; int64_t first_bad; } chk_ctx;
+
+static void chk_range(void* p, int64_t i0, int64_t i1)
+{
+    chk_ctx* c = (chk_ctx*)p;
+    int64_t bad = 0, first = -1;
+    for (int64_t i = i0; i < i1; ++i) {
+        uint32_t bits = (uint32_t)(c->start + (uint64_t)i);
+        float x; memcpy(&x, &bits, 4);
+        int want = fmt_encode(&F_HIF8, (double)x, c->sat);
+        if (want != c->got[i]) { if (first < 0) first = i; ++bad; }
+    }
+    if (bad) {
+        __atomic_fetch_add(&c->bad, bad, __ATOMIC_RELAXED);
+        int64_t cur = __atomic_load_n(&c->first_bad, __ATOMIC_RELAXED);
+        while ((cur < 0 || first < cur) &&
+               !__atomic_compare_exchange_n(&c->first_bad, &cur, first, 0, __ATOMIC_RELAXED, __ATOMIC_RELAXED)) {}
+    }
+}
+
+/* Compares codes[i] against the encoding of the fp32 bit pattern start + i,
+ * for i < count.  Returns the number of mismatches; *first_bad gets the
+ * first mismatching index (or -1). */
+int64_t orc_hif8_check_patterns(uint64_t start, int64_t count, const uint8_t* codes, int saturate,
+                                int nthreads, int64_t* first_bad)
+{
+    chk_ctx c = { start, codes, saturate, 0, -1 };
+    parallel_for(count, nthreads, 1 << 18, chk_range, &c);
+    if (first_bad) *first_bad = c.first_bad;
+    return c.bad;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Powers of two in 8 bits                                                   */
+/* ------------------------------------------------------------------------ */
+
+/* IEEE binary16 rounding (to nearest even, subnormals, overflow to Inf),
+ * the FP16 carrier of Alg. 2. */
+double orc_round_fp16(double y)
+{
+    if (isnan(y) || isinf(y) || y == 0.0) return y;
+    double a = fabs(y);
+    int e;
+    frexp(a, &e);                      /* a = f * 2^e with f in [0.5, 1) */
+    int ue = e - 1;                    /* unbiased exponent of a */
+    if (ue < -14) ue = -14;            /* subnormal spacing is 2^-24 */
+    double q = ldexp(1.0, ue - 10);    /* spacing of binary16 at a */
+    double r = nearbyint(a / q) * q;   /* default rounding mode: ties to even */
+    if (r > 65504.0) r = INFINITY;
+    return copysign(r, y);
+}
+
+/* E8(t) = HiF8(2^t) for a HiF8 value t (R5). */
+static double e8_hif8(double t)
+{
+    if (isnan(t)) return t;
+    if (t == -INFINITY) return 0.0;
+    double y = exp2(t);
+    if (isinf(y)) y = 1.0e308;         /* a finite overflow, saturated below */
+    return fmt_round(&F_HIF8, y, 1);
+}
+
+/* The 256-entry table code -> code of HiF8(2^decode(code)).
+ * variant 0: fp64 exp2 with one HiF8 rounding (R5).
+ * variant 1: Alg. 2 literally, with FP16 as the carrier of the exp2 result. */
+void orc_exp2_table(uint8_t out[256], int variant)
+{
+    for (int c = 0; c < 256; ++c) {
+        double x = orc_hif8_decode(c);
+        if (isnan(x)) { out[c] = (uint8_t)F_HIF8.nan_code; continue; }
+        if (x == INFINITY) { out[c] = (uint8_t)F_HIF8.inf_code; continue; }
+        if (x == -INFINITY) { out[c] = 0; continue; }
+        if (variant == 0) {
+            out[c] = (uint8_t)fmt_encode(&F_HIF8, e8_hif8(x), 1);
+        } else {
+            /* x is a HiF8 value, so the FP16 -> HiF8 -> FP16 steps leave it unchanged */
+            double y16 = orc_round_fp16(exp2(x));       /* exp2 evaluated in FP16 */
+            out[c] = (uint8_t)fmt_encode(&F_HIF8, y16, 1);
+        }
+    }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Attention                                                                 */
+/* ------------------------------------------------------------------------ */
+
+enum {
+    ORC_E2E_HIF8 = 0,       /* Alg. 1 (the "E2E HiF8" setup)                      */
+    ORC_DEFAULT = 1,        /* eq. (2), softmax in fp32 ("Default")                */
+    ORC_EXP2_HIF8 = 2,      /* eq. (2), every power of two in HiF8 ("Exp2 HiF8")   */
+    ORC_NAIVE_E2E = 3,      /* eq. (2) on scores cast to HiF8 first ("Naive E2E")  */
+    ORC_EXP2_E4M3 = 4,      /* Table 1 ablations: input/output formats of exp2     */
+    ORC_EXP2_E5M2 = 5,
+    ORC_EXP2_E4M3xE5M2 = 6,
+    ORC_E2E_EXACT = 7       /* Alg. 1 control flow with the 8-bit casts removed and
+                               all arithmetic in fp64 (quantizer off)              */
+};
+
+typedef struct {
+    const uint16_t *q, *k, *v;
+    int B, Hq, Hkv, Sq, Sk, D, causal, block;
+    int mode, lambda, n_b0, literal_else;
+    float c32;              /* log2(e)/sqrt(D) (or the override), as fp32 */
+    double c64;             /* the same scale in fp64 (for ORC_E2E_EXACT and eq. (1)) */
+    const int64_t* rows;
+    double *o, *lse;
+    int32_t* nrestart;      /* restarted B1 blocks per row (nullable) */
+} attn_job;
+
+static inline double bf16_to_double(uint16_t b)
+{
+    uint32_t u = (uint32_t)b << 16;
+    float f; memcpy(&f, &u, 4);
+    return (double)f;
+}
+
+static inline int last_visible_key(const attn_job* J, int r)
+{
+    if (!J->causal) return J->Sk - 1;
+    int kmax = r + J->Sk - J->Sq;               /* R11: bottom-right alignment */
+    return kmax < J->Sk - 1 ? kmax : J->Sk - 1;
+}
+
+/* q.k of a query row and a key row, summed in fp64 (exact products) */
+static double dot64(const uint16_t* a, const uint16_t* b, int D)
+{
+    double s = 0.0;
+    for (int i = 0; i < D; ++i) s += bf16_to_double(a[i]) * bf16_to_double(b[i]);
+    return s;
+}
+
+typedef struct { double* acc; double* ot; double* pv; double* qrow; } row_scratch;
+
+/* One query row of Alg. 1.  acc_c = fl32(q.k_c); the block loop is the B0
+ * loop for j < n_b0 and the B1 loop afterwards. */
+static void row_alg1(const attn_job* J, int b, int h, int r, row_scratch* W,
+                     double* o, double* lse, int32_t* nrs)
+{
+    const int D = J->D, blk = J->block;
+    const int g = h / (J->Hq / J->Hkv);                                   /* R17 */
+    const uint16_t* qr = J->q + (((int64_t)b * J->Hq + h) * J->Sq + r) * D;
+    const uint16_t* kb = J->k + ((int64_t)b * J->Hkv + g) * (int64_t)J->Sk * D;
+    const uint16_t* vb = J->v + ((int64_t)b * J->Hkv + g) * (int64_t)J->Sk * D;
+    const int exact = (J->mode == ORC_E2E_EXACT);
+    const int kmax = last_visible_key(J, r);
+    const int nblk = kmax < 0 ? 0 : kmax / blk + 1;
+    double m = -INFINITY, d = 0.0;
+    int32_t restarts = 0;
+    for (int i = 0; i < D; ++i) W->ot[i] = 0.0;
+
+    for (int j = 0; j < nblk; ++j) {
+        const int c0 = j * blk;
+        const int c1 = (c0 + blk <= kmax + 1) ? c0 + blk : kmax + 1;   /* visible keys of block j */
+        const int nc = c1 - c0;
+        /* S_i^(j) = Q_i K_j^T * log2(e)/sqrt(d): keep acc, the unscaled dot product */
+        for (int c = 0; c < nc; ++c) {
+            double a = dot64(qr, kb + (int64_t)(c0 + c) * D, D);
+            W->acc[c] = exact ? a : (double)(float)a;                   /* R15 */
+        }
+        int restart;
+        double m_new = m, ref = m;
+        if (j < J->n_b0) {
+            restart = 1;                                                 /* B0 loop (R9) */
+        } else {
+            /* B1 loop: m~ = m^(j-1); T = S - rowfill(m~) in 8-bit; restart if
+             * ceil(rowmax T) > lambda */
+            double tmax = -INFINITY;
+            for (int c = 0; c < nc; ++c) {
+                double t;
+                if (exact) t = W->acc[c] * J->c64 - m;
+                else t = orc_hif8_round((double)fmaf((float)W->acc[c], J->c32, (float)(-m)), 1);
+                if (t > tmax) tmax = t;
+            }
+            restart = ceil(tmax) > (double)J->lambda;
+            if (!restart) {
+                m_new = m + fmax(0.0, ceil(tmax));
+                ref = m;                                                 /* m~ stays m^(j-1) */
+            } else {
+                ++restarts;
+            }
+        }
+        if (restart) {
+            /* S in high precision; m^(j) = max(m^(j-1), ceil(rowmax S)); m~ = m^(j) */
+            double M = -INFINITY;
+            for (int c = 0; c < nc; ++c) {
+                double s = exact ? W->acc[c] * J->c64 : (double)((float)W->acc[c] * J->c32);
+                if (s > M) M = s;
+            }
+            m_new = fmax(m, ceil(M));
+            ref = m_new;
+        }
+        /* P = 2^T in 8-bit, T = S - rowfill(m~) in 8-bit (eq. 3) */
+        double rowsum = 0.0;
+        for (int i = 0; i < D; ++i) W->pv[i] = 0.0;
+        for (int c = 0; c < nc; ++c) {
+            double p;
+            if (exact) p = exp2(W->acc[c] * J->c64 - ref);
+            else {
+                double t = orc_hif8_round((double)fmaf((float)W->acc[c], J->c32, (float)(-ref)), 1);
+                p = e8_hif8(t);
+            }
+            if (p == 0.0) continue;
+            rowsum += p;
+            const uint16_t* vr = vb + (int64_t)(c0 + c) * D;
+            for (int i = 0; i < D; ++i) W->pv[i] += p * bf16_to_double(vr[i]);
+        }
+        /* d and O~ with the exact integer powers of two of Sec. 3.3 (R7) */
+        const double alpha = (m == -INFINITY) ? 0.0 : exp2(m - m_new);
+        const double beta = (J->literal_else && !restart) ? 1.0 : exp2(ref - m_new);
+        d = alpha * d + beta * rowsum;
+        for (int i = 0; i < D; ++i) W->ot[i] = alpha * W->ot[i] + beta * W->pv[i];
+        m = m_new;
+    }
+    if (nblk == 0) {
+        for (int i = 0; i < D; ++i) o[i] = 0.0;
+        *lse = -INFINITY;
+    } else {
+        for (int i = 0; i < D; ++i) o[i] = W->ot[i] / d;                 /* O = diag(d)^-1 O~ */
+        *lse = M_LN2 * (m + log2(d));                                     /* R13 */
+    }
+    if (nrs) *nrs = restarts;
+}
+
+/* One query row of eq. (2) in the setups of Sec. 4.1 / Table 1 that keep the
+ * real-valued running maximum: Default, Exp2 HiF8, Naive E2E, Exp2 FP8.
+ * The softmax runs in fp32 as the Default setup states. */
+static void row_eq2(const attn_job* J, int b, int h, int r, row_scratch* W, double* o, double* lse)
+{
+    const int D = J->D, blk = J->block;
+    const int g = h / (J->Hq / J->Hkv);
+    const uint16_t* qr = J->q + (((int64_t)b * J->Hq + h) * J->Sq + r) * D;
+    const uint16_t* kb = J->k + ((int64_t)b * J->Hkv + g) * (int64_t)J->Sk * D;
+    const uint16_t* vb = J->v + ((int64_t)b * J->Hkv + g) * (int64_t)J->Sk * D;
+    const int kmax = last_visible_key(J, r);
+    const int nblk = kmax < 0 ? 0 : kmax / blk + 1;
+    const orc_format *fin = &F_HIF8, *fout = &F_HIF8;
+    if (J->mode == ORC_EXP2_E4M3) { fin = &F_E4M3; fout = &F_E4M3; }
+    if (J->mode == ORC_EXP2_E5M2) { fin = &F_E5M2; fout = &F_E5M2; }
+    if (J->mode == ORC_EXP2_E4M3xE5M2) { fin = &F_E4M3; fout = &F_E5M2; }
+    float m = -INFINITY, d = 0.0f;
+    float* ot = (float*)W->pv;                                           /* fp32 O~ */
+    for (int i = 0; i < D; ++i) ot[i] = 0.0f;
+
+    for (int j = 0; j < nblk; ++j) {
+        const int c0 = j * blk;
+        const int c1 = (c0 + blk <= kmax + 1) ? c0 + blk : kmax + 1;
+        const int nc = c1 - c0;
+        float rowmax = -INFINITY;
+        for (int c = 0; c < nc; ++c) {
+            float s = (float)dot64(qr, kb + (int64_t)(c0 + c) * D, D) * J->c32;
+            if (J->mode == ORC_NAIVE_E2E) s = (float)fmt_round(&F_HIF8, s, 1);   /* scores cast first */
+            W->acc[c] = s;
+            if (s > rowmax) rowmax = s;
+        }
+        const float m_new = m > rowmax ? m : rowmax;                     /* m^(j) */
+        float alpha;
+        if (m == -INFINITY) alpha = 0.0f;
+        else if (J->mode == ORC_DEFAULT) alpha = exp2f(m - m_new);
+        else alpha = (float)fmt_round(fout, exp2(fmt_round(fin, (double)(m - m_new), 1)), 1);
+        float rowsum = 0.0f;
+        d *= alpha;
+        for (int i = 0; i < D; ++i) ot[i] *= alpha;
+        for (int c = 0; c < nc; ++c) {
+            float x = (float)W->acc[c] - m_new;
+            float p;
+            if (J->mode == ORC_DEFAULT) p = exp2f(x);
+            else p = (float)fmt_round(fout, exp2(fmt_round(fin, (double)x, 1)), 1);
+            rowsum += p;
+            const uint16_t* vr = vb + (int64_t)(c0 + c) * D;
+            for (int i = 0; i < D; ++i) ot[i] += p * (float)bf16_to_double(vr[i]);
+        }
+        d += rowsum;
+        m = m_new;
+    }
+    if (nblk == 0) {
+        for (int i = 0; i < D; ++i) o[i] = 0.0;
+        *lse = -INFINITY;
+    } else {
+        for (int i = 0; i < D; ++i) o[i] = (double)(ot[i] / d);
+        *lse = M_LN2 * ((double)m + log2((double)d));
+    }
+}
+
+/* eq. (1) in fp64: O = softmax(Q K^T / sqrt(d)) V (scale from c64 when overridden) */
+static void row_exact(const attn_job* J, int b, int h, int r, row_scratch* W, double* o, double* lse)
+{
+    const int D = J->D;
+    const int g = h / (J->Hq / J->Hkv);
+    const uint16_t* qr = J->q + (((int64_t)b * J->Hq + h) * J->Sq + r) * D;
+    const uint16_t* kb = J->k + ((int64_t)b * J->Hkv + g) * (int64_t)J->Sk * D;
+    const uint16_t* vb = J->v + ((int64_t)b * J->Hkv + g) * (int64_t)J->Sk * D;
+    const int kmax = last_visible_key(J, r);
+    const double scale = J->c64 * M_LN2;                                 /* natural units */
+    if (kmax < 0) {
+        for (int i = 0; i < D; ++i) o[i] = 0.0;
+        *lse = -INFINITY;
+        return;
+    }
+    double smax = -INFINITY;
+    for (int c = 0; c <= kmax; ++c) {
+        double s = dot64(qr, kb + (int64_t)c * D, D) * scale;
+        W->acc[c] = s;
+        if (s > smax) smax = s;
+    }
+    double z = 0.0;
+    for (int i = 0; i < D; ++i) W->ot[i] = 0.0;
+    for (int c = 0; c <= kmax; ++c) {
+        double w = exp(W->acc[c] - smax);
+        z += w;
+        const uint16_t* vr = vb + (int64_t)c * D;
+        for (int i = 0; i < D; ++i) W->ot[i] += w * bf16_to_double(vr[i]);
+    }
+    for (int i = 0; i < D; ++i) o[i] = W->ot[i] / z;
+    *lse = smax + log(z);
+}
+
+typedef struct { attn_job* J; int which; } attn_ctx;   /* which: 0 modes, 1 exact */
+
+static void attn_range(void* p, int64_t i0, int64_t i1)
+{
+    attn_ctx* C = (attn_ctx*)p;
+    attn_job* J = C->J;
+    const int D = J->D;
+    row_scratch W;
+    size_t nacc = (size_t)(C->which ? (J->Sk > J->block ? J->Sk : J->block) : J->block);
+    W.acc = (double*)malloc(sizeof(double) * (nacc + 1));
+    W.ot = (double*)malloc(sizeof(double) * D);
+    W.pv = (double*)malloc(sizeof(double) * D);
+    W.qrow = NULL;
+    for (int64_t i = i0; i < i1; ++i) {
+        int64_t g = J->rows[i];
+        int r = (int)(g % J->Sq);
+        int h = (int)((g / J->Sq) % J->Hq);
+        int b = (int)(g / ((int64_t)J->Sq * J->Hq));
+        double* o = J->o + i * D;
+        double* lse = J->lse + i;
+        if (C->which) row_exact(J, b, h, r, &W, o, lse);
+        else if (J->mode == ORC_E2E_HIF8 || J->mode == ORC_E2E_EXACT)
+            row_alg1(J, b, h, r, &W, o, lse, J->nrestart ? J->nrestart + i : NULL);
+        else row_eq2(J, b, h, r, &W, o, lse);
+    }
+    free(W.acc); free(W.ot); free(W.pv);
+}
+
+static int attn_check(int B, int Hq, int Hkv, int Sq, int Sk, int D, int block)
+{
+    if (B < 0 || Hq <= 0 || Hkv <= 0 || Sq < 0 || Sk < 0 || D <= 0 || block <= 0) return 1;
+    if (Hq % Hkv) return 1;
+    return 0;
+}
+
+/* rows: global query-row indices (b*Hq + h)*Sq + r; outputs o[nrows*D], lse[nrows].
+ * scale_log2 = 0 selects log2(e)/sqrt(D).  Returns 0 or 1 (bad arguments). */
+int orc_attention(const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                  int B, int Hq, int Hkv, int Sq, int Sk, int D, int causal, int block,
+                  int mode, int lambda, int n_b0, int literal_else, double scale_log2,
+                  const int64_t* rows, int64_t nrows, double* o, double* lse, int32_t* nrestart,
+                  int nthreads)
+{
+    if (attn_check(B, Hq, Hkv, Sq, Sk, D, block) || mode < 0 || mode > 7) return 1;
+    attn_job J = { q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, block, mode, lambda, n_b0,
+                   literal_else, 0.0f, 0.0, rows, o, lse, nrestart };
+    J.c64 = scale_log2 != 0.0 ? scale_log2 : M_LOG2E / sqrt((double)D);
+    J.c32 = (float)J.c64;
+    if (mode != ORC_E2E_EXACT) J.c64 = (double)J.c32;
+    attn_ctx C = { &J, 0 };
+    parallel_for(nrows, nthreads, 1, attn_range, &C);
+    return 0;
+}
+
+int orc_exact_attention(const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                        int B, int Hq, int Hkv, int Sq, int Sk, int D, int causal,
+                        double scale_log2, const int64_t* rows, int64_t nrows,
+                        double* o, double* lse, int nthreads)
+{
+    if (attn_check(B, Hq, Hkv, Sq, Sk, D, 1)) return 1;
+    attn_job J = { q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, 1, 0, 0, 0, 0, 0.0f, 0.0,
+                   rows, o, lse, NULL };
+    J.c64 = scale_log2 != 0.0 ? scale_log2 : M_LOG2E / sqrt((double)D);
+    attn_ctx C = { &J, 1 };
+    parallel_for(nrows, nthreads, 1, attn_range, &C);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* The vector-side steps of Alg. 1 on given scores                           */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+    const float* s; int64_t cols, ld; int block, lambda, n_b0;
+    uint8_t* codes; int32_t* ref_shift; double *m_out, *d_out; uint8_t* restarted;
+} sb_job;
+
+static void sb_range(void* p, int64_t i0, int64_t i1)
+{
+    sb_job* J = (sb_job*)p;
+    const int64_t nblk = (J->cols + J->block - 1) / J->block;
+    double* refs = (double*)malloc(sizeof(double) * (size_t)(nblk ? nblk : 1));
+    for (int64_t r = i0; r < i1; ++r) {
+        const float* S = J->s + r * J->ld;
+        uint8_t* code = J->codes + r * J->cols;
+        double m = -INFINITY, d = 0.0;
+        for (int64_t j = 0; j < nblk; ++j) {
+            const int64_t c0 = j * J->block;
+            const int64_t c1 = c0 + J->block < J->cols ? c0 + J->block : J->cols;
+            int restart;
+            double m_new = m, ref = m;
+            if (j < J->n_b0) restart = 1;
+            else {
+                double tmax = -INFINITY;
+                for (int64_t c = c0; c < c1; ++c) {
+                    if (S[c] == -INFINITY) continue;                     /* masked score */
+                    double t = orc_hif8_round((double)(S[c] - (float)m), 1);
+                    if (t > tmax) tmax = t;
+                }
+                restart = ceil(tmax) > (double)J->lambda;
+                if (!restart) m_new = m + fmax(0.0, ceil(tmax));
+            }
+            if (restart) {
+                double M = -INFINITY;
+                for (int64_t c = c0; c < c1; ++c) if ((double)S[c] > M) M = S[c];
+                m_new = fmax(m, ceil(M));
+                ref = m_new;
+            }
+            double rowsum = 0.0;
+            for (int64_t c = c0; c < c1; ++c) {
+                double p = 0.0;
+                if (ref != -INFINITY && S[c] != -INFINITY)
+                    p = e8_hif8(orc_hif8_round((double)(S[c] - (float)ref), 1));
+                code[c] = (uint8_t)fmt_encode(&F_HIF8, p, 1);
+                rowsum += p;
+            }
+            const double alpha = (m == -INFINITY) ? 0.0 : exp2(m - m_new);
+            const double beta = (ref == -INFINITY) ? 0.0 : exp2(ref - m_new);
+            d = alpha * d + beta * rowsum;
+            m = m_new;
+            refs[j] = ref;
+            if (J->restarted) J->restarted[r * nblk + j] = (uint8_t)restart;
+        }
+        for (int64_t j = 0; j < nblk; ++j)
+            J->ref_shift[r * nblk + j] = (refs[j] == -INFINITY) ? INT32_MIN : (int32_t)(refs[j] - m);
+        J->m_out[r] = m;
+        J->d_out[r] = d;
+    }
+    free(refs);
+}
+
+/* s: rows x cols fp32 scores in log2 units (row stride ld); -inf marks a
+ * masked score.  Outputs: codes[rows*cols] (HiF8 code of P relative to its
+ * block's reference), ref_shift[rows*nblk] = ref_j - m_final (INT32_MIN for a
+ * block with no finite reference), m_final, d_final, restarted[rows*nblk]. */
+int orc_softmax_block(const float* s, int64_t rows, int64_t cols, int64_t ld, int block,
+                      int lambda, int n_b0, uint8_t* codes, int32_t* ref_shift,
+                      double* m_final, double* d_final, uint8_t* restarted, int nthreads)
+{
+    if (rows < 0 || cols < 0 || block <= 0 || ld < cols) return 1;
+    sb_job J = { s, cols, ld, block, lambda, n_b0, codes, ref_shift, m_final, d_final, restarted };
+    parallel_for(rows, nthreads, 8, sb_range, &J);
+    return 0;
+}
