@@ -1,0 +1,162 @@
+"""Benchmark of the fused BAPS attention forward on one MI355X.
+
+A step is one fused forward pass (every step of Alg. 1: QK^T, block-aware
+rescaling, HiF8 quantisation, 8-bit exp2, online max/sum, PV) over one batch
+of synthetic input already resident in HBM.  Default workload: the
+Llama-3-8B-shaped causal prefill (B=1, Hq=32, Hkv=8, S=4096, D=128, block
+128, outlier channels).  Prints ONE JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "BAPS attention fwd TFLOP/s + % bf16 MFMA peak (prefill); decode HBM GB/s"
+PEAK_BF16_TFLOPS = 2500.0        # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0            # MI355X HBM3E
+KERNEL_SRC = os.path.join(ROOT, "paper_2602_02071_amd", "csrc", "attn_fwd.hip")
+
+
+def _src_hash(path):
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+
+
+def _traffic(kernel_tag):
+    """HBM bytes per launch from the committed rocprofv3 counter summary,
+    if it was taken on the current kernel source (else None)."""
+    path = os.path.join(ROOT, "profiles", f"{kernel_tag}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path))
+    except ValueError:
+        return None
+    if rec.get("source_sha256_16") != _src_hash(KERNEL_SRC):
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def _time_launches(fn, steps, warmup):
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    st = torch.cuda.current_stream()
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    t0 = time.perf_counter()
+    for i in range(steps):
+        starts[i].record(st)
+        fn()
+        ends[i].record(st)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = [s.elapsed_time(e) for s, e in zip(starts, ends)]
+    return wall, per
+
+
+def run_attention(cfg, steps, warmup):
+    import torch
+    import paper_2602_02071_amd as baps
+    from paper_2602_02071_amd.workloads import make_workload
+    w, q, k, v = make_workload(cfg)
+    dev = torch.device("cuda:0")
+    qt, kt, vt = (torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).to(dev) for x in (q, k, v))
+    o = torch.empty((w.B, w.Hq, w.Sq, w.D), dtype=torch.float32, device=dev)
+    lse = torch.empty((w.B, w.Hq, w.Sq), dtype=torch.float32, device=dev)
+    baps.baps_init()
+    stream = torch.cuda.current_stream().cuda_stream
+
+    def step():
+        baps.baps_attention_fwd(qt, kt, vt, o, lse, w.B, w.Hq, w.Hkv, w.Sq, w.Sk, w.D, w.causal, w.block, stream)
+
+    wall, per = _time_launches(step, steps, warmup)
+    return w, (q, k, v), wall, per
+
+
+def cpu_baseline(w, qkv, seconds_hint=True):
+    """The oracle, as it stands, on a bounded sample of the same workload."""
+    import oracle
+    from paper_2602_02071_amd.workloads import sample_rows
+    q, k, v = qkv
+    heads = range(0, w.Hq, 2) if w.Sq > 1 else range(w.Hq)
+    rows = sample_rows(w, every=1, tile=1, heads=heads) if w.Sq > 1 else None
+    if w.Sq == 1:
+        rows = np.arange(0, w.B * w.Hq, 8, dtype=np.int64)
+    nthreads = oracle.default_threads()
+    t0 = time.perf_counter()
+    oracle.attention(q, k, v, w.B, w.Hq, w.Hkv, w.Sq, w.Sk, w.D, w.causal, w.block, rows=rows,
+                     nthreads=nthreads)
+    dt = time.perf_counter() - t0
+    r = rows % w.Sq
+    vis = np.minimum(w.Sk, r + w.Sk - w.Sq + 1) if w.causal else np.full(r.shape, w.Sk)
+    flops = 4.0 * w.D * float(np.clip(vis, 0, w.Sk).sum())
+    sample = (f"{len(rows)} of {w.B * w.Hq * w.Sq} query rows ({'every other head, all rows' if w.Sq > 1 else 'every 8th row'})"
+              f", {dt:.1f} s")
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": nthreads, "kind": "oracle", "sample": sample}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=2, help="workload 1..5 (2 = Llama-3-8B prefill)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-decode", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
+              "BAPS attention shards over (batch, KV head) with no exchange, see the design notes",
+              file=sys.stderr)
+        sys.exit(2)
+
+    w, qkv, wall, per = run_attention(args.config, args.steps, args.warmup)
+    ms = wall * 1e3 / args.steps
+    avg_launch_ms = float(np.mean(per))
+    flops = w.flops
+    tflops = flops / (ms * 1e-3) / 1e12
+    achieved = flops / (avg_launch_ms * 1e-3) / 1e12
+    decode_bound = w.Sq == 1
+    if decode_bound:
+        gbs = w.bytes_qkvo / (avg_launch_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": gbs / PEAK_HBM_GBS,
+                "traffic": _traffic("attn_fwd_decode")}
+    else:
+        roof = {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": achieved / PEAK_BF16_TFLOPS, "traffic": _traffic("attn_fwd_prefill")}
+    out = {
+        "metric": METRIC,
+        "value": tflops if not decode_bound else w.bytes_qkvo / (ms * 1e-3) / 1e9,
+        "unit": "TFLOP/s" if not decode_bound else "GB/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "Sq": w.Sq, "Sk": w.Sk, "D": w.D,
+                   "causal": w.causal, "block": w.block, "lambda": 1, "n_b0": 1, "softmax": "hif8",
+                   "tokens_per_s": w.B * w.Sq / (ms * 1e-3)},
+        "roofline": roof,
+    }
+    if not args.no_decode and args.config != 3:
+        wd, _, wall_d, per_d = run_attention(3, max(5, args.steps // 2), 2)
+        ms_d = float(np.mean(per_d))
+        gbs = wd.bytes_qkvo / (ms_d * 1e-3) / 1e9
+        out["decode"] = {"workload": wd.name, "ms_per_step": ms_d, "value": gbs, "unit": "GB/s",
+                         "frac_of_hbm_peak": gbs / PEAK_HBM_GBS, "tokens_per_s": wd.B / (ms_d * 1e-3),
+                         "traffic": _traffic("attn_fwd_decode")}
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, qkv)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,131 @@
+/*
+ * BAPS attention on AMD Instinct MI355X (gfx950): C ABI.
+ *
+ * The library computes the attention forward pass of "BAPS: A Fine-Grained
+ * Low-Precision Scheme for Softmax in Attention via Block-Aware Precision
+ * reScaling" (arXiv 2602.02071): attention as stated in eq. (1), evaluated
+ * blockwise by the base-2 online softmax of eq. (2) reorganised as Alg. 1
+ * ("E2E HiF8"): the score minus an integer reference maximum is cast to the
+ * 8-bit HiF8 format (eq. 3), its power of two is taken in HiF8 (App. A,
+ * Alg. 2), and the running denominator and output are rescaled by exact
+ * integer powers of two (Sec. 3.3).
+ *
+ * Conventions for every entry point:
+ *  - Tensor pointers are DEVICE pointers owned by the caller; the library
+ *    never allocates, frees or retains them.  Inputs are not modified;
+ *    outputs are fully overwritten.
+ *  - Every call is asynchronous on `stream` (a hipStream_t passed as void*;
+ *    NULL is the default stream) and does not synchronise, except the very
+ *    first call on a device, which uploads the library's read-only 32 KiB
+ *    score table to that device synchronously (baps_init does it up front).
+ *  - Layouts are contiguous row-major: q, o [B][Hq][Sq][D]; k, v
+ *    [B][Hkv][Sk][D]; lse [B][Hq][Sq].  bf16 tensors are passed as raw
+ *    16-bit patterns.
+ *  - Return value: BAPS_OK (0), BAPS_INVALID_ARGUMENT (1: a null pointer
+ *    where one is required, a negative size, Hq not a multiple of Hkv),
+ *    BAPS_UNSUPPORTED (2: a head dimension or block size without a kernel),
+ *    BAPS_HIP_ERROR (3: the HIP runtime reported an error at launch).
+ *    baps_status_string() names a status.  No exception crosses the ABI.
+ *  - Empty work (B, Hq or Sq zero; n or rows zero) returns BAPS_OK and
+ *    touches nothing.
+ */
+#ifndef BAPS_H
+#define BAPS_H
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define BAPS_OK 0
+#define BAPS_INVALID_ARGUMENT 1
+#define BAPS_UNSUPPORTED 2
+#define BAPS_HIP_ERROR 3
+
+#define BAPS_HIF8_SATURATE 1
+
+/*
+ * Fused BAPS attention forward, canonical setup ("E2E HiF8", Sec. 4.1):
+ * restart threshold lambda = 1, B0 = the first key block, Alg. 1 per query
+ * row, HiF8 rounding to nearest with ties away from zero, saturating.
+ *
+ * q [B,Hq,Sq,D], k/v [B,Hkv,Sk,D] bf16; o [B,Hq,Sq,D] fp32; lse [B,Hq,Sq]
+ * fp32, natural log of the softmax denominator of the scores q.k/sqrt(D),
+ * as the HiF8 pipeline estimates it: ln2 * (m + log2 d); may be NULL.
+ * Query head h reads key/value head h / (Hq/Hkv).  causal != 0 masks key c
+ * from query row r when c > r + Sk - Sq (bottom-right aligned); a row that
+ * sees no key gets o = 0 and lse = -inf.  block is the key tile of Alg. 1
+ * (the unit of the restart test and of the integer maximum).
+ * Supported: D in {64, 128}; block in {32, 64, 128}.  Sk may be 0.
+ */
+int baps_attention_fwd(const void* q, const void* k, const void* v, float* o, float* lse,
+                       int B, int Hq, int Hkv, int Sq, int Sk, int D, int causal, int block,
+                       void* stream);
+
+/* Knobs of Alg. 1 and the paper's ablations (Sec. 4.1, Table 4). */
+typedef struct {
+    int lambda;                          /* restart threshold (integer, Alg. 1); 1 canonical  */
+    int n_b0;                            /* key blocks in B0 (taken first, Alg. 1); 1 canonical */
+    float scale_log2;                    /* score scale in log2 units; 0 => log2(e)/sqrt(D)    */
+    unsigned long long* restart_counts;  /* device [B*Hq][2]: restarted and visited B1 row-
+                                            blocks (accumulated with atomics; the caller
+                                            zeroes it); NULL to skip                          */
+} baps_params_t;
+
+/* baps_attention_fwd with explicit knobs; p must not be NULL; scale_log2
+ * must be >= 0. */
+int baps_attention_fwd_ex(const void* q, const void* k, const void* v, float* o, float* lse,
+                          int B, int Hq, int Hkv, int Sq, int Sk, int D, int causal, int block,
+                          const baps_params_t* p, void* stream);
+
+/*
+ * HiF8 codec (the 8-bit format used by every 8-bit step of the method;
+ * Sec. 2, App. A).  hif8_encode: codes[i] = code of the HiF8 value nearest
+ * to x[i] (ties away from zero).  flags: BAPS_HIF8_SATURATE clamps finite
+ * overflow to +-2^15 (else values from 1.25*2^15 up become +-Inf); no other
+ * bit may be set.  +-Inf -> 0x6F/0xEF, NaN -> 0x80, values that round to
+ * zero -> 0x00.  hif8_decode: x[i] = value of codes[i] (0x80 -> NaN).
+ * n >= 0 elements; any alignment (16-byte aligned buffers stream faster).
+ */
+int hif8_encode(const float* x, unsigned char* codes, long long n, int flags, void* stream);
+int hif8_decode(const unsigned char* codes, float* x, long long n, void* stream);
+
+/*
+ * The vector-side steps of Alg. 1 on fp32 score rows already in log2 units
+ * (S of eq. 2), one sequential pass over the key blocks of each row:
+ * block maximum, B0 / restart rule with threshold lambda, integer running
+ * maximum (Sec. 3.3), T = HiF8(S - ref), P = HiF8(2^T), and the running
+ * denominator.  s: rows x cols, row stride ld_s >= cols (elements); -inf
+ * marks a masked score; scores must be finite or -inf.
+ * Outputs (device):
+ *   p_codes  [rows, cols]  HiF8 code of P relative to its block's reference
+ *   ref_shift[rows, nblk]  ref_j - m_final (<= 0); INT32_MIN for a block
+ *                          with no finite reference; nblk = ceil(cols/block)
+ *   m_final  [rows]        final integer maximum (-inf for an all-masked row)
+ *   d_final  [rows]        final denominator, relative to 2^m_final
+ *   restarted[rows, nblk]  1 where the block took the high-precision path
+ *                          (B0 or a restart); may be NULL
+ * The normalised probability of score c in block j is
+ *   decode(p_codes[r,c]) * 2^ref_shift[r,j] / d_final[r].
+ * block must be one of 64, 128, 256, 512, 1024.  flags must be 0.
+ */
+int baps_softmax_block(const float* s, long long rows, long long cols, long long ld_s, int block,
+                       int lambda, int n_b0, int flags, unsigned char* p_codes, int* ref_shift,
+                       float* m_final, float* d_final, unsigned char* restarted, void* stream);
+
+/* Host copy of the library's 8-bit exp2 table: out_codes[c] = code of
+ * HiF8(2^decode(c)) (App. A, Alg. 2, with exp2 in double precision).
+ * Needs no GPU. */
+int baps_get_exp2_lut(unsigned char out_codes[256]);
+
+/* Uploads the score table to the current device (synchronously).  Optional:
+ * the first call of an entry point on a device does it otherwise. */
+int baps_init(void);
+
+/* Text of a status code (static storage). */
+const char* baps_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BAPS_H */

@@ -1,0 +1,148 @@
+"""BAPS attention on MI355X: Python binding of libbaps.so.
+
+The names match the C ABI in include/baps.h.  This module only marshals
+arguments (tensor -> device pointer, stream -> handle, status -> exception);
+every step of the method runs in the library's HIP kernels.  PyTorch is used
+for device memory and streams only.  If the library has not been built the
+calls raise: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libbaps.so")
+
+BAPS_OK = 0
+BAPS_INVALID_ARGUMENT = 1
+BAPS_UNSUPPORTED = 2
+BAPS_HIP_ERROR = 3
+BAPS_HIF8_SATURATE = 1
+
+EXPORTS = ("baps_attention_fwd", "baps_attention_fwd_ex", "hif8_encode", "hif8_decode",
+           "baps_softmax_block", "baps_get_exp2_lut", "baps_init", "baps_status_string")
+
+_lib = None
+
+
+class BapsError(RuntimeError):
+    def __init__(self, fn, status):
+        super().__init__(f"{fn}: {status_string(status)} (status {status})")
+        self.status = status
+
+
+class baps_params_t(ctypes.Structure):
+    _fields_ = [("lambda_", ctypes.c_int), ("n_b0", ctypes.c_int), ("scale_log2", ctypes.c_float),
+                ("restart_counts", ctypes.c_void_p)]
+
+
+def load():
+    """Load libbaps.so (raises when it is missing: build it first)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: run __graft_entry__.build() (hipcc, gfx950) first")
+    L = ctypes.CDLL(LIB_PATH)
+    P, I, LL = ctypes.c_void_p, ctypes.c_int, ctypes.c_longlong
+    L.baps_attention_fwd.argtypes = [P, P, P, P, P, I, I, I, I, I, I, I, I, P]
+    L.baps_attention_fwd_ex.argtypes = [P, P, P, P, P, I, I, I, I, I, I, I, I,
+                                        ctypes.POINTER(baps_params_t), P]
+    L.hif8_encode.argtypes = [P, P, LL, I, P]
+    L.hif8_decode.argtypes = [P, P, LL, P]
+    L.baps_softmax_block.argtypes = [P, LL, LL, LL, I, I, I, I, P, P, P, P, P, P]
+    L.baps_get_exp2_lut.argtypes = [P]
+    L.baps_init.argtypes = []
+    L.baps_status_string.argtypes = [I]
+    L.baps_status_string.restype = ctypes.c_char_p
+    for name in EXPORTS[:-1]:
+        getattr(L, name).restype = I
+    _lib = L
+    return L
+
+
+def status_string(status: int) -> str:
+    return load().baps_status_string(int(status)).decode()
+
+
+def _p(x):
+    """Device pointer of a tensor (or an int / None passed through)."""
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _check(fn, st):
+    if st != BAPS_OK:
+        raise BapsError(fn, st)
+
+
+def baps_attention_fwd(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, stream=None):
+    _check("baps_attention_fwd", load().baps_attention_fwd(
+        _p(q), _p(k), _p(v), _p(o), _p(lse), B, Hq, Hkv, Sq, Sk, D, int(causal), block, _stream(stream)))
+
+
+def baps_attention_fwd_ex(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, lam=1, n_b0=1,
+                          scale_log2=0.0, restart_counts=None, stream=None):
+    prm = baps_params_t(int(lam), int(n_b0), float(scale_log2), _p(restart_counts))
+    _check("baps_attention_fwd_ex", load().baps_attention_fwd_ex(
+        _p(q), _p(k), _p(v), _p(o), _p(lse), B, Hq, Hkv, Sq, Sk, D, int(causal), block,
+        ctypes.byref(prm), _stream(stream)))
+
+
+def hif8_encode(x, codes, n, flags=BAPS_HIF8_SATURATE, stream=None):
+    _check("hif8_encode", load().hif8_encode(_p(x), _p(codes), n, flags, _stream(stream)))
+
+
+def hif8_decode(codes, x, n, stream=None):
+    _check("hif8_decode", load().hif8_decode(_p(codes), _p(x), n, _stream(stream)))
+
+
+def baps_softmax_block(s, rows, cols, ld_s, block, lam, n_b0, flags, p_codes, ref_shift, m_final, d_final,
+                       restarted=None, stream=None):
+    _check("baps_softmax_block", load().baps_softmax_block(
+        _p(s), rows, cols, ld_s, block, lam, n_b0, flags, _p(p_codes), _p(ref_shift), _p(m_final),
+        _p(d_final), _p(restarted), _stream(stream)))
+
+
+def baps_get_exp2_lut():
+    buf = (ctypes.c_ubyte * 256)()
+    _check("baps_get_exp2_lut", load().baps_get_exp2_lut(buf))
+    return bytes(buf)
+
+
+def baps_init():
+    _check("baps_init", load().baps_init())
+
+
+# ------------------------------------------------------------ tensor helpers
+def attention(q, k, v, causal, block, lse=True, lam=None, n_b0=None, scale_log2=0.0, restart_counts=None,
+              stream=None):
+    """Allocate O (and lse) with torch on q's device and run the fused pass.
+    q [B,Hq,Sq,D], k/v [B,Hkv,Sk,D] bf16 CUDA tensors, contiguous."""
+    import torch
+    B, Hq, Sq, D = q.shape
+    Hkv, Sk = k.shape[1], k.shape[2]
+    for t in (q, k, v):
+        if t.dtype != torch.bfloat16 or not t.is_contiguous() or not t.is_cuda:
+            raise ValueError("q, k, v must be contiguous bf16 device tensors")
+    o = torch.empty((B, Hq, Sq, D), dtype=torch.float32, device=q.device)
+    l = torch.empty((B, Hq, Sq), dtype=torch.float32, device=q.device) if lse else None
+    if lam is None and n_b0 is None and not scale_log2 and restart_counts is None:
+        baps_attention_fwd(q, k, v, o, l, B, Hq, Hkv, Sq, Sk, D, causal, block, stream)
+    else:
+        baps_attention_fwd_ex(q, k, v, o, l, B, Hq, Hkv, Sq, Sk, D, causal, block,
+                              1 if lam is None else lam, 1 if n_b0 is None else n_b0, scale_log2,
+                              restart_counts, stream)
+    return o, l

@@ -1,0 +1,217 @@
+// C ABI of the BAPS HIP library: argument validation, the read-only score
+// table, and dispatch to the kernels.  No allocation on any call path.
+#include <cmath>
+#include <cstring>
+#include <mutex>
+
+#include "../../include/baps.h"
+#include "common.hpp"
+
+namespace {
+
+using namespace baps;
+
+// The score table: entry i covers every fp32 value whose bits 31..19 equal
+// i.  P = HiF8(2^HiF8(T)) (App. A: the power of two evaluated on the 8-bit
+// input and rounded back to 8 bits), as fp32 bits with the HiF8 code of P
+// in the low byte.  Lives in static device memory, one copy per device.
+__device__ uint32_t g_score_table[kTabEntries];
+
+// HiF8 value of a double, rounded once: truncating to fp32 toward zero keeps
+// the sign, the exponent and the leading mantissa bits that decide a
+// round-to-nearest-away HiF8 result.
+float hif8_round_double(double y)
+{
+    if (std::isnan(y)) return std::nanf("");
+    float f = (float)y;
+    if (std::isinf(y)) return f;
+    if (std::fabs((double)f) > std::fabs(y)) f = std::nextafterf(f, 0.0f);
+    return hif8::round(f, true);
+}
+
+// 2^t for a HiF8 value t, rounded to HiF8 (saturating: 2^t beyond 2^15 gives 2^15)
+float hif8_exp2(float t)
+{
+    if (std::isnan(t)) return t;
+    if (t == -INFINITY) return 0.0f;
+    if (t == INFINITY) return t;
+    double y = std::exp2((double)t);
+    if (std::isinf(y)) y = 1.0e300;
+    return hif8_round_double(y);
+}
+
+struct Table {
+    uint32_t e[kTabEntries];
+    Table()
+    {
+        for (uint32_t i = 0; i < (uint32_t)kTabEntries; ++i) {
+            const float T = hif8::u2f(i << kTabShift);
+            const float p = hif8_exp2(hif8::round(T, true));
+            const uint32_t pb = hif8::f2u(p);
+            e[i] = (pb & 0xffffff00u) | hif8::encode(p, true);
+        }
+    }
+};
+
+const Table& host_table()
+{
+    static Table t;
+    return t;
+}
+
+constexpr int kMaxDevices = 64;
+std::mutex g_mutex;
+const uint32_t* g_dev_table[kMaxDevices] = {};
+
+int table_on_current_device(const uint32_t** out)
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return BAPS_HIP_ERROR;
+    if (dev < 0 || dev >= kMaxDevices) return BAPS_UNSUPPORTED;
+    std::lock_guard<std::mutex> lock(g_mutex);
+    if (!g_dev_table[dev]) {
+        const Table& t = host_table();
+        if (hipMemcpyToSymbol(HIP_SYMBOL(g_score_table), t.e, sizeof(t.e), 0, hipMemcpyHostToDevice) != hipSuccess)
+            return BAPS_HIP_ERROR;
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(g_score_table)) != hipSuccess || !ptr) return BAPS_HIP_ERROR;
+        g_dev_table[dev] = static_cast<const uint32_t*>(ptr);
+    }
+    *out = g_dev_table[dev];
+    return BAPS_OK;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+int status_of(hipError_t e) { return e == hipSuccess ? BAPS_OK : BAPS_HIP_ERROR; }
+
+int attention_impl(const void* q, const void* k, const void* v, float* o, float* lse, int B, int Hq,
+                   int Hkv, int Sq, int Sk, int D, int causal, int block, int lambda, int n_b0,
+                   float scale_log2, unsigned long long* counters, void* stream)
+{
+    if (B < 0 || Hq < 0 || Hkv < 0 || Sq < 0 || Sk < 0 || n_b0 < 0) return BAPS_INVALID_ARGUMENT;
+    if (!(scale_log2 >= 0.0f) || std::isinf(scale_log2)) return BAPS_INVALID_ARGUMENT;
+    if (B == 0 || Hq == 0 || Sq == 0) return BAPS_OK;
+    if (Hkv == 0 || Hq % Hkv != 0) return BAPS_INVALID_ARGUMENT;
+    if (!q || !o || (Sk > 0 && (!k || !v))) return BAPS_INVALID_ARGUMENT;
+    if (!aligned16(q) || !aligned16(o) || (Sk > 0 && (!aligned16(k) || !aligned16(v))))
+        return BAPS_INVALID_ARGUMENT;
+    if (!(D == 64 || D == 128) || !(block == 32 || block == 64 || block == 128)) return BAPS_UNSUPPORTED;
+    if ((long long)Sq * (Hq / Hkv) > 0x7fffffffLL || Hkv > 65535 || B > 65535) return BAPS_UNSUPPORTED;
+    const uint32_t* tab = nullptr;
+    int st = table_on_current_device(&tab);
+    if (st) return st;
+    AttnParams p;
+    p.q = static_cast<const uint16_t*>(q);
+    p.k = static_cast<const uint16_t*>(k);
+    p.v = static_cast<const uint16_t*>(v);
+    p.o = o;
+    p.lse = lse;
+    p.tab = tab;
+    p.counters = counters;
+    p.B = B; p.Hq = Hq; p.Hkv = Hkv; p.Sq = Sq; p.Sk = Sk;
+    p.causal = causal ? 1 : 0;
+    p.lambda = lambda;
+    p.n_b0 = n_b0;
+    p.c = scale_log2 > 0.0f ? scale_log2 : (float)(1.4426950408889634 / std::sqrt((double)D));
+    return status_of(launch_attention(p, D, block, static_cast<hipStream_t>(stream)));
+}
+
+}  // namespace
+
+extern "C" {
+
+int baps_attention_fwd(const void* q, const void* k, const void* v, float* o, float* lse, int B, int Hq,
+                       int Hkv, int Sq, int Sk, int D, int causal, int block, void* stream)
+{
+    try {
+        return attention_impl(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, 1, 1, 0.0f, nullptr,
+                              stream);
+    } catch (...) {
+        return BAPS_HIP_ERROR;
+    }
+}
+
+int baps_attention_fwd_ex(const void* q, const void* k, const void* v, float* o, float* lse, int B, int Hq,
+                          int Hkv, int Sq, int Sk, int D, int causal, int block, const baps_params_t* prm,
+                          void* stream)
+{
+    if (!prm) return BAPS_INVALID_ARGUMENT;
+    try {
+        return attention_impl(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, prm->lambda, prm->n_b0,
+                              prm->scale_log2, prm->restart_counts, stream);
+    } catch (...) {
+        return BAPS_HIP_ERROR;
+    }
+}
+
+int hif8_encode(const float* x, unsigned char* codes, long long n, int flags, void* stream)
+{
+    if (n < 0 || (flags & ~BAPS_HIF8_SATURATE)) return BAPS_INVALID_ARGUMENT;
+    if (n == 0) return BAPS_OK;
+    if (!x || !codes) return BAPS_INVALID_ARGUMENT;
+    return status_of(launch_hif8_encode(x, codes, n, (flags & BAPS_HIF8_SATURATE) != 0,
+                                        static_cast<hipStream_t>(stream)));
+}
+
+int hif8_decode(const unsigned char* codes, float* x, long long n, void* stream)
+{
+    if (n < 0) return BAPS_INVALID_ARGUMENT;
+    if (n == 0) return BAPS_OK;
+    if (!x || !codes) return BAPS_INVALID_ARGUMENT;
+    return status_of(launch_hif8_decode(codes, x, n, static_cast<hipStream_t>(stream)));
+}
+
+int baps_softmax_block(const float* s, long long rows, long long cols, long long ld_s, int block, int lambda,
+                       int n_b0, int flags, unsigned char* p_codes, int* ref_shift, float* m_final,
+                       float* d_final, unsigned char* restarted, void* stream)
+{
+    if (rows < 0 || cols < 0 || ld_s < cols || n_b0 < 0 || flags != 0) return BAPS_INVALID_ARGUMENT;
+    if (!(block == 64 || block == 128 || block == 256 || block == 512 || block == 1024)) return BAPS_UNSUPPORTED;
+    if (rows == 0) return BAPS_OK;
+    if (!m_final || !d_final || (cols > 0 && (!s || !p_codes || !ref_shift))) return BAPS_INVALID_ARGUMENT;
+    if (rows > 4LL * 0x7fffffffLL) return BAPS_UNSUPPORTED;
+    try {
+        const uint32_t* tab = nullptr;
+        int st = table_on_current_device(&tab);
+        if (st) return st;
+        SoftmaxBlockParams p;
+        p.s = s; p.rows = rows; p.cols = cols; p.ld = ld_s;
+        p.block = block; p.lambda = lambda; p.n_b0 = n_b0;
+        p.codes = p_codes; p.ref_shift = ref_shift; p.m_final = m_final; p.d_final = d_final;
+        p.restarted = restarted; p.tab = tab;
+        return status_of(launch_softmax_block(p, static_cast<hipStream_t>(stream)));
+    } catch (...) {
+        return BAPS_HIP_ERROR;
+    }
+}
+
+int baps_get_exp2_lut(unsigned char out_codes[256])
+{
+    if (!out_codes) return BAPS_INVALID_ARGUMENT;
+    for (int c = 0; c < 256; ++c) out_codes[c] = hif8::encode(hif8_exp2(hif8::decode((uint8_t)c)), true);
+    return BAPS_OK;
+}
+
+int baps_init(void)
+{
+    try {
+        const uint32_t* tab = nullptr;
+        return table_on_current_device(&tab);
+    } catch (...) {
+        return BAPS_HIP_ERROR;
+    }
+}
+
+const char* baps_status_string(int status)
+{
+    switch (status) {
+    case BAPS_OK: return "ok";
+    case BAPS_INVALID_ARGUMENT: return "invalid argument";
+    case BAPS_UNSUPPORTED: return "unsupported shape or option";
+    case BAPS_HIP_ERROR: return "HIP runtime error";
+    default: return "unknown status";
+    }
+}
+
+}  // extern "C"

@@ -1,0 +1,75 @@
+// Shared device-side helpers and launch descriptors of the BAPS HIP library.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "hif8.hpp"
+
+namespace baps {
+
+typedef __bf16 bf16x8 __attribute__((__vector_size__(8 * sizeof(__bf16))));
+typedef float f32x16 __attribute__((__vector_size__(16 * sizeof(float))));
+typedef float f32x4 __attribute__((__vector_size__(4 * sizeof(float))));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// Entries of the score table, indexed by bits 31..19 of an fp32 value T:
+// P = HiF8(2^HiF8(T)) as fp32 bits in bits 31..8, and the HiF8 code of P in
+// bits 7..0 (every HiF8 value has at most 3 mantissa bits, so bits 19..0 of
+// its fp32 pattern are zero).  The upper 16 bits are P in bf16, exactly.
+constexpr int kTabEntries = 8192;
+constexpr int kTabShift = 19;
+
+struct AttnParams {
+    const uint16_t* q;          // [B, Hq, Sq, D] bf16
+    const uint16_t* k;          // [B, Hkv, Sk, D] bf16
+    const uint16_t* v;          // [B, Hkv, Sk, D] bf16
+    float* o;                   // [B, Hq, Sq, D]
+    float* lse;                 // [B, Hq, Sq] or null
+    const uint32_t* tab;        // score table (device)
+    unsigned long long* counters;  // [B*Hq][2] restarted / visited B1 row-blocks, or null
+    int B, Hq, Hkv, Sq, Sk;
+    int causal, lambda, n_b0;
+    float c;                    // log2(e)/sqrt(D) as fp32 (or the caller's override)
+};
+
+struct SoftmaxBlockParams {
+    const float* s;
+    long long rows, cols, ld;
+    int block, lambda, n_b0;
+    uint8_t* codes;
+    int32_t* ref_shift;
+    float* m_final;
+    float* d_final;
+    uint8_t* restarted;
+    const uint32_t* tab;
+};
+
+// exact 2^k for an integer-valued float k (0 below the fp32 range)
+__device__ __forceinline__ float exp2_int(float k)
+{
+    if (k < -160.0f) return 0.0f;
+    return ldexpf(1.0f, (int)k);
+}
+
+__device__ __forceinline__ float wave_max(float v)
+{
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
+    return v;
+}
+
+__device__ __forceinline__ float wave_sum(float v)
+{
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+    return v;
+}
+
+// Host launchers (one per kernel family); return a hipError_t.
+hipError_t launch_hif8_encode(const float* x, uint8_t* codes, long long n, bool saturate, hipStream_t st);
+hipError_t launch_hif8_decode(const uint8_t* codes, float* x, long long n, hipStream_t st);
+hipError_t launch_softmax_block(const SoftmaxBlockParams& p, hipStream_t st);
+hipError_t launch_attention(const AttnParams& p, int D, int block, hipStream_t st);
+
+}  // namespace baps

@@ -1,0 +1,84 @@
+"""The C-ABI library loads, exports every symbol include/baps.h declares, and
+rejects bad arguments before touching the GPU (CPU only)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle as O
+import paper_2602_02071_amd as baps
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "baps.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(\w+)\s*\(", src, flags=re.M)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(baps.LIB_PATH):
+        pytest.fail("libbaps.so is not built (run __graft_entry__.build())")
+    return baps.load()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = _declared()
+    assert set(names) >= {"baps_attention_fwd", "baps_attention_fwd_ex", "hif8_encode", "hif8_decode",
+                          "baps_softmax_block", "baps_get_exp2_lut"}
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(baps.EXPORTS) == set(names)
+
+
+def test_exp2_lut_matches_oracle(lib):
+    lut = np.frombuffer(baps.baps_get_exp2_lut(), dtype=np.uint8)
+    assert np.array_equal(lut, O.exp2_table(0))
+
+
+def test_status_strings(lib):
+    assert baps.status_string(0) == "ok"
+    assert "invalid" in baps.status_string(1)
+    assert "unsupported" in baps.status_string(2)
+    assert baps.status_string(99) == "unknown status"
+
+
+def _attn(lib, q=16, k=16, v=16, o=16, B=1, Hq=2, Hkv=1, Sq=8, Sk=8, D=64, causal=0, block=64):
+    return lib.baps_attention_fwd(q, k, v, o, None, B, Hq, Hkv, Sq, Sk, D, causal, block, None)
+
+
+def test_attention_argument_checks(lib):
+    assert _attn(lib, B=-1) == 1
+    assert _attn(lib, Sk=-3) == 1
+    assert _attn(lib, Hq=3, Hkv=2) == 1
+    assert _attn(lib, Hkv=0) == 1
+    assert _attn(lib, q=None) == 1
+    assert _attn(lib, o=None) == 1
+    assert _attn(lib, q=18) == 1                 # q not 16-byte aligned
+    assert _attn(lib, D=96) == 2
+    assert _attn(lib, block=48) == 2
+    assert _attn(lib, B=0) == 0                  # empty work
+    assert _attn(lib, Sq=0, q=None, o=None) == 0
+    prm = baps.baps_params_t(1, 1, -1.0, None)
+    assert lib.baps_attention_fwd_ex(16, 16, 16, 16, None, 1, 1, 1, 4, 4, 64, 0, 64, ctypes.byref(prm), None) == 1
+    assert lib.baps_attention_fwd_ex(16, 16, 16, 16, None, 1, 1, 1, 4, 4, 64, 0, 64, None, None) == 1
+
+
+def test_codec_and_softmax_block_argument_checks(lib):
+    assert lib.hif8_encode(16, 16, -1, 1, None) == 1
+    assert lib.hif8_encode(16, 16, 10, 4, None) == 1
+    assert lib.hif8_encode(None, 16, 10, 1, None) == 1
+    assert lib.hif8_encode(None, None, 0, 1, None) == 0
+    assert lib.hif8_decode(16, None, 10, None) == 1
+    assert lib.hif8_decode(None, None, 0, None) == 0
+    sb = lib.baps_softmax_block
+    assert sb(16, 4, 100, 99, 64, 1, 1, 0, 16, 16, 16, 16, None, None) == 1      # ld < cols
+    assert sb(16, 4, 100, 100, 96, 1, 1, 0, 16, 16, 16, 16, None, None) == 2     # block
+    assert sb(16, 4, 100, 100, 64, 1, 1, 3, 16, 16, 16, 16, None, None) == 1     # flags
+    assert sb(16, 4, 100, 100, 64, 1, -1, 0, 16, 16, 16, 16, None, None) == 1    # n_b0
+    assert sb(None, 4, 100, 100, 64, 1, 1, 0, 16, 16, 16, 16, None, None) == 1
+    assert sb(None, 0, 100, 100, 64, 1, 1, 0, None, None, None, None, None, None) == 0
