@@ -84,6 +84,9 @@ def _load():
     L.orc_attention.restype = i32
     L.orc_attention.argtypes = [P, P, P, i32, i32, i32, i32, i32, i32, i32, i32,
                                 i32, i32, i32, i32, d, P, i64, P, P, P, i32]
+    L.orc_attention_ex.restype = i32
+    L.orc_attention_ex.argtypes = [P, P, P, i32, i32, i32, i32, i32, i32, i32, i32,
+                                   i32, i32, i32, i32, d, P, i64, P, P, P, P, d, ctypes.c_uint64, i32]
     L.orc_exact_attention.restype = i32
     L.orc_exact_attention.argtypes = [P, P, P, i32, i32, i32, i32, i32, i32, i32,
                                       d, P, i64, P, P, i32]
@@ -185,12 +188,18 @@ def _rows(rows, total):
 
 
 def attention(q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, block, mode=E2E_HIF8, lam=1, n_b0=1,
-              literal_else=False, scale_log2=0.0, rows=None, nthreads=0):
+              literal_else=False, scale_log2=0.0, rows=None, nthreads=0, margin=False, jitter=0.0,
+              jitter_seed=0):
     """Attention rows in one of the paper's setups.
 
     q: [B,Hq,Sq,D], k/v: [B,Hkv,Sk,D] bf16 bit patterns.  rows: global row
     indices (b*Hq + h)*Sq + r (all rows when None).  Returns (o[n,D] fp64,
-    lse[n] fp64, restarts[n] int32 -- restarted B1 blocks per row)."""
+    lse[n] fp64, restarts[n] int32 -- restarted B1 blocks per row), plus the
+    per-row decision margin when margin=True: how far the row's 8-bit
+    decisions sit from a rounding boundary, in units of the fp32 dot-product
+    accumulation error bound (>= 1: every valid high-precision S yields this
+    result).  jitter moves every dot product by jitter times that bound
+    (same direction for jitter_seed 0, random signs otherwise)."""
     L = _load()
     q, k, v = _bits(q), _bits(k), _bits(v)
     rows = _rows(rows, B * Hq * Sq)
@@ -198,11 +207,15 @@ def attention(q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, block, mode=E2E_HIF8, lam=
     o = np.zeros((n, D), dtype=np.float64)
     lse = np.zeros(n, dtype=np.float64)
     nrs = np.zeros(n, dtype=np.int32)
-    st = L.orc_attention(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, Sq, Sk, D, int(causal), block,
-                         int(mode), int(lam), int(n_b0), int(literal_else), float(scale_log2),
-                         _ptr(rows), n, _ptr(o), _ptr(lse), _ptr(nrs), int(nthreads))
+    mg = np.zeros(n, dtype=np.float64) if margin else None
+    st = L.orc_attention_ex(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, Sq, Sk, D, int(causal), block,
+                            int(mode), int(lam), int(n_b0), int(literal_else), float(scale_log2),
+                            _ptr(rows), n, _ptr(o), _ptr(lse), _ptr(nrs), _ptr(mg), float(jitter),
+                            ctypes.c_uint64(int(jitter_seed)), int(nthreads))
     if st:
         raise ValueError("oracle rejected the attention arguments")
+    if margin:
+        return o, lse, nrs, mg
     return o, lse, nrs
 
 

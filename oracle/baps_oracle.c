@@ -361,6 +361,9 @@ typedef struct {
     const int64_t* rows;
     double *o, *lse;
     int32_t* nrestart;      /* restarted B1 blocks per row (nullable) */
+    double* margin;         /* decision margin per row (nullable), see row_alg1 */
+    double jitter;          /* move each dot product by jitter * its error bound */
+    uint64_t jitter_seed;   /* 0: every dot product moves the same way; else random signs */
 } attn_job;
 
 static inline double bf16_to_double(uint16_t b)
@@ -385,12 +388,65 @@ static double dot64(const uint16_t* a, const uint16_t* b, int D)
     return s;
 }
 
-typedef struct { double* acc; double* ot; double* pv; double* qrow; } row_scratch;
+/* A matrix unit accumulating q.k in fp32 lands within ACC_ERR * 2^-24 *
+ * sum_d |q_d k_d| of the exact dot product (the measured worst case on
+ * gfx950 bf16 MFMA is about 6 of these units).  Every high-precision S
+ * within that bound is an equally valid "S in high precision" of Alg. 1. */
+#define ACC_ERR 16.0
 
-/* One query row of Alg. 1.  acc_c = fl32(q.k_c); the block loop is the B0
- * loop for j < n_b0 and the B1 loop afterwards. */
+static double abs_dot64(const uint16_t* a, const uint16_t* b, int D)
+{
+    double s = 0.0;
+    for (int i = 0; i < D; ++i) s += fabs(bf16_to_double(a[i]) * bf16_to_double(b[i]));
+    return s;
+}
+
+static uint64_t splitmix64(uint64_t x)
+{
+    x += 0x9E3779B97F4A7C15ull;
+    x = (x ^ (x >> 30)) * 0xBF58476D1CE4E5B9ull;
+    x = (x ^ (x >> 27)) * 0x94D049BB133111EBull;
+    return x ^ (x >> 31);
+}
+
+/* Distance from x to the nearest point where the HiF8 rounding of x changes. */
+static double hif8_boundary_distance(double x)
+{
+    const orc_format* f = &F_HIF8;
+    double a = fabs(x);
+    int top = f->n - 1;
+    if (a >= f->val[top]) return a - 0.5 * (f->val[top - 1] + f->val[top]);
+    int lo = 0, hi = top;
+    while (hi - lo > 1) {
+        int mid = (lo + hi) / 2;
+        if (f->val[mid] <= a) lo = mid; else hi = mid;
+    }
+    double up = 0.5 * (f->val[lo] + f->val[lo + 1]) - a;
+    if (up < 0) up = -up;
+    double down = lo > 0 ? a - 0.5 * (f->val[lo - 1] + f->val[lo]) : up;
+    if (down < 0) down = -down;
+    return up < down ? up : down;
+}
+
+static double integer_distance(double x)
+{
+    double a = x - floor(x), b = ceil(x) - x;
+    return a < b ? a : b;
+}
+
+typedef struct { double *acc, *eps, *ot, *pv, *ref, *bmargin; } row_scratch;
+
+/* One query row of Alg. 1.  acc_c = fl32(q.k_c) (R15); the block loop is
+ * the B0 loop for j < n_b0 and the B1 loop afterwards.
+ *
+ * With J->margin set, the row also reports how far its 8-bit decisions sit
+ * from a boundary, in units of the accumulation error bound of each score:
+ * the HiF8 rounding of every T that carries weight >= 2^-12 of the final
+ * maximum, the restart test of every B1 block, and the ceil of the row
+ * maximum of every block that takes the high-precision path.  A margin of
+ * at least 1 means every valid high-precision S gives this same result. */
 static void row_alg1(const attn_job* J, int b, int h, int r, row_scratch* W,
-                     double* o, double* lse, int32_t* nrs)
+                     double* o, double* lse, int32_t* nrs, double* margin_out)
 {
     const int D = J->D, blk = J->block;
     const int g = h / (J->Hq / J->Hkv);                                   /* R17 */
@@ -400,18 +456,34 @@ static void row_alg1(const attn_job* J, int b, int h, int r, row_scratch* W,
     const int exact = (J->mode == ORC_E2E_EXACT);
     const int kmax = last_visible_key(J, r);
     const int nblk = kmax < 0 ? 0 : kmax / blk + 1;
+    const uint64_t rowid = (((uint64_t)b * J->Hq + h) * J->Sq + r);
     double m = -INFINITY, d = 0.0;
     int32_t restarts = 0;
     for (int i = 0; i < D; ++i) W->ot[i] = 0.0;
 
+    /* S = Q K^T * log2(e)/sqrt(d): keep acc, the unscaled dot product */
+    for (int c = 0; c <= kmax; ++c) {
+        const uint16_t* kr = kb + (int64_t)c * D;
+        double a = dot64(qr, kr, D);
+        const double e_acc = ACC_ERR * ldexp(abs_dot64(qr, kr, D), -24);
+        if (J->jitter != 0.0) {
+            double sgn = 1.0;
+            if (J->jitter_seed) sgn = (splitmix64(J->jitter_seed ^ (rowid * 1000003ull + (uint64_t)c)) & 1) ? 1.0 : -1.0;
+            a += J->jitter * sgn * e_acc;
+        }
+        W->acc[c] = exact ? a : (double)(float)a;
+        W->eps[c] = e_acc * J->c64;                                      /* in S units */
+    }
+
     for (int j = 0; j < nblk; ++j) {
         const int c0 = j * blk;
         const int c1 = (c0 + blk <= kmax + 1) ? c0 + blk : kmax + 1;   /* visible keys of block j */
+        const double* acc = W->acc + c0;
         const int nc = c1 - c0;
-        /* S_i^(j) = Q_i K_j^T * log2(e)/sqrt(d): keep acc, the unscaled dot product */
+        double bm = INFINITY, eps_blk = 0.0, amax = -INFINITY;
         for (int c = 0; c < nc; ++c) {
-            double a = dot64(qr, kb + (int64_t)(c0 + c) * D, D);
-            W->acc[c] = exact ? a : (double)(float)a;                   /* R15 */
+            if (W->eps[c0 + c] > eps_blk) eps_blk = W->eps[c0 + c];
+            if (acc[c] > amax) amax = acc[c];
         }
         int restart;
         double m_new = m, ref = m;
@@ -423,11 +495,16 @@ static void row_alg1(const attn_job* J, int b, int h, int r, row_scratch* W,
             double tmax = -INFINITY;
             for (int c = 0; c < nc; ++c) {
                 double t;
-                if (exact) t = W->acc[c] * J->c64 - m;
-                else t = orc_hif8_round((double)fmaf((float)W->acc[c], J->c32, (float)(-m)), 1);
+                if (exact) t = acc[c] * J->c64 - m;
+                else t = orc_hif8_round((double)fmaf((float)acc[c], J->c32, (float)(-m)), 1);
                 if (t > tmax) tmax = t;
             }
             restart = ceil(tmax) > (double)J->lambda;
+            if (m != -INFINITY) {
+                double x = amax * J->c64 - m;
+                double dist = hif8_boundary_distance(x) / eps_blk;
+                if (dist < bm) bm = dist;
+            }
             if (!restart) {
                 m_new = m + fmax(0.0, ceil(tmax));
                 ref = m;                                                 /* m~ stays m^(j-1) */
@@ -439,20 +516,22 @@ static void row_alg1(const attn_job* J, int b, int h, int r, row_scratch* W,
             /* S in high precision; m^(j) = max(m^(j-1), ceil(rowmax S)); m~ = m^(j) */
             double M = -INFINITY;
             for (int c = 0; c < nc; ++c) {
-                double s = exact ? W->acc[c] * J->c64 : (double)((float)W->acc[c] * J->c32);
+                double s = exact ? acc[c] * J->c64 : (double)((float)acc[c] * J->c32);
                 if (s > M) M = s;
             }
             m_new = fmax(m, ceil(M));
             ref = m_new;
+            double dist = integer_distance(amax * J->c64) / eps_blk;
+            if (dist < bm) bm = dist;
         }
         /* P = 2^T in 8-bit, T = S - rowfill(m~) in 8-bit (eq. 3) */
         double rowsum = 0.0;
         for (int i = 0; i < D; ++i) W->pv[i] = 0.0;
         for (int c = 0; c < nc; ++c) {
             double p;
-            if (exact) p = exp2(W->acc[c] * J->c64 - ref);
+            if (exact) p = exp2(acc[c] * J->c64 - ref);
             else {
-                double t = orc_hif8_round((double)fmaf((float)W->acc[c], J->c32, (float)(-ref)), 1);
+                double t = orc_hif8_round((double)fmaf((float)acc[c], J->c32, (float)(-ref)), 1);
                 p = e8_hif8(t);
             }
             if (p == 0.0) continue;
@@ -466,6 +545,26 @@ static void row_alg1(const attn_job* J, int b, int h, int r, row_scratch* W,
         d = alpha * d + beta * rowsum;
         for (int i = 0; i < D; ++i) W->ot[i] = alpha * W->ot[i] + beta * W->pv[i];
         m = m_new;
+        W->ref[j] = ref;
+        W->bmargin[j] = bm;
+    }
+    if (margin_out) {
+        double mg = INFINITY;
+        if (!exact) {
+            for (int j = 0; j < nblk; ++j) {
+                if (W->bmargin[j] < mg) mg = W->bmargin[j];
+                const int c0 = j * blk;
+                const int c1 = (c0 + blk <= kmax + 1) ? c0 + blk : kmax + 1;
+                for (int c = c0; c < c1; ++c) {
+                    double x = W->acc[c] * J->c64 - W->ref[j];
+                    double p = e8_hif8(orc_hif8_round((double)fmaf((float)W->acc[c], J->c32, (float)(-W->ref[j])), 1));
+                    if (ldexp(p, (int)(W->ref[j] - m)) < 1.0 / 4096.0) continue;
+                    double dist = hif8_boundary_distance(x) / W->eps[c];
+                    if (dist < mg) mg = dist;
+                }
+            }
+        }
+        *margin_out = mg;
     }
     if (nblk == 0) {
         for (int i = 0; i < D; ++i) o[i] = 0.0;
@@ -578,11 +677,14 @@ static void attn_range(void* p, int64_t i0, int64_t i1)
     attn_job* J = C->J;
     const int D = J->D;
     row_scratch W;
-    size_t nacc = (size_t)(C->which ? (J->Sk > J->block ? J->Sk : J->block) : J->block);
-    W.acc = (double*)malloc(sizeof(double) * (nacc + 1));
+    const size_t nkeys = (size_t)(J->Sk > J->block ? J->Sk : J->block) + 1;
+    const size_t nblk = (size_t)(J->Sk / J->block) + 2;
+    W.acc = (double*)malloc(sizeof(double) * nkeys);
+    W.eps = (double*)malloc(sizeof(double) * nkeys);
     W.ot = (double*)malloc(sizeof(double) * D);
     W.pv = (double*)malloc(sizeof(double) * D);
-    W.qrow = NULL;
+    W.ref = (double*)malloc(sizeof(double) * nblk);
+    W.bmargin = (double*)malloc(sizeof(double) * nblk);
     for (int64_t i = i0; i < i1; ++i) {
         int64_t g = J->rows[i];
         int r = (int)(g % J->Sq);
@@ -592,10 +694,11 @@ static void attn_range(void* p, int64_t i0, int64_t i1)
         double* lse = J->lse + i;
         if (C->which) row_exact(J, b, h, r, &W, o, lse);
         else if (J->mode == ORC_E2E_HIF8 || J->mode == ORC_E2E_EXACT)
-            row_alg1(J, b, h, r, &W, o, lse, J->nrestart ? J->nrestart + i : NULL);
+            row_alg1(J, b, h, r, &W, o, lse, J->nrestart ? J->nrestart + i : NULL,
+                     J->margin ? J->margin + i : NULL);
         else row_eq2(J, b, h, r, &W, o, lse);
     }
-    free(W.acc); free(W.ot); free(W.pv);
+    free(W.acc); free(W.eps); free(W.ot); free(W.pv); free(W.ref); free(W.bmargin);
 }
 
 static int attn_check(int B, int Hq, int Hkv, int Sq, int Sk, int D, int block)
@@ -606,22 +709,37 @@ static int attn_check(int B, int Hq, int Hkv, int Sq, int Sk, int D, int block)
 }
 
 /* rows: global query-row indices (b*Hq + h)*Sq + r; outputs o[nrows*D], lse[nrows].
- * scale_log2 = 0 selects log2(e)/sqrt(D).  Returns 0 or 1 (bad arguments). */
-int orc_attention(const uint16_t* q, const uint16_t* k, const uint16_t* v,
-                  int B, int Hq, int Hkv, int Sq, int Sk, int D, int causal, int block,
-                  int mode, int lambda, int n_b0, int literal_else, double scale_log2,
-                  const int64_t* rows, int64_t nrows, double* o, double* lse, int32_t* nrestart,
-                  int nthreads)
+ * scale_log2 = 0 selects log2(e)/sqrt(D).  margin (nullable): per-row decision
+ * margin of the E2E HiF8 setup (see row_alg1).  jitter / jitter_seed move every
+ * dot product by jitter times its accumulation error bound (all the same way
+ * for seed 0, random signs otherwise): another valid high-precision S.
+ * Returns 0 or 1 (bad arguments). */
+int orc_attention_ex(const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                     int B, int Hq, int Hkv, int Sq, int Sk, int D, int causal, int block,
+                     int mode, int lambda, int n_b0, int literal_else, double scale_log2,
+                     const int64_t* rows, int64_t nrows, double* o, double* lse, int32_t* nrestart,
+                     double* margin, double jitter, uint64_t jitter_seed, int nthreads)
 {
     if (attn_check(B, Hq, Hkv, Sq, Sk, D, block) || mode < 0 || mode > 7) return 1;
     attn_job J = { q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, block, mode, lambda, n_b0,
-                   literal_else, 0.0f, 0.0, rows, o, lse, nrestart };
+                   literal_else, 0.0f, 0.0, rows, o, lse, nrestart, margin, jitter, jitter_seed };
     J.c64 = scale_log2 != 0.0 ? scale_log2 : M_LOG2E / sqrt((double)D);
     J.c32 = (float)J.c64;
     if (mode != ORC_E2E_EXACT) J.c64 = (double)J.c32;
     attn_ctx C = { &J, 0 };
     parallel_for(nrows, nthreads, 1, attn_range, &C);
     return 0;
+}
+
+int orc_attention(const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                  int B, int Hq, int Hkv, int Sq, int Sk, int D, int causal, int block,
+                  int mode, int lambda, int n_b0, int literal_else, double scale_log2,
+                  const int64_t* rows, int64_t nrows, double* o, double* lse, int32_t* nrestart,
+                  int nthreads)
+{
+    return orc_attention_ex(q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, block, mode, lambda, n_b0,
+                            literal_else, scale_log2, rows, nrows, o, lse, nrestart, NULL, 0.0, 0,
+                            nthreads);
 }
 
 int orc_exact_attention(const uint16_t* q, const uint16_t* k, const uint16_t* v,
@@ -631,7 +749,7 @@ int orc_exact_attention(const uint16_t* q, const uint16_t* k, const uint16_t* v,
 {
     if (attn_check(B, Hq, Hkv, Sq, Sk, D, 1)) return 1;
     attn_job J = { q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, 1, 0, 0, 0, 0, 0.0f, 0.0,
-                   rows, o, lse, NULL };
+                   rows, o, lse, NULL, NULL, 0.0, 0 };
     J.c64 = scale_log2 != 0.0 ? scale_log2 : M_LOG2E / sqrt((double)D);
     attn_ctx C = { &J, 1 };
     parallel_for(nrows, nthreads, 1, attn_range, &C);

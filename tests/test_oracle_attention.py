@@ -247,3 +247,20 @@ def test_restarts_fall_as_lambda_grows(peaked):
     args, _ = peaked
     counts = [O.attention(*args, 128, lam=lam)[2].sum() for lam in (0, 1, 2, 4)]
     assert all(a >= b for a, b in zip(counts, counts[1:])) and counts[0] > counts[-1]
+
+
+def test_margin_marks_rows_stable_under_valid_scores():
+    # a row whose decisions all clear their rounding boundaries by the
+    # accumulation error bound keeps its result for every valid
+    # high-precision S; ambiguous rows exist and may move
+    args = _args(1, 4, 2, 200, 400, 128, True, seed=13, outliers=True)
+    o, _, _, mg = O.attention(*args, 32, margin=True)
+    det = mg >= 1
+    assert det.sum() > 0.8 * det.size
+    moved_amb = 0
+    for scale, seed in ((1.0, 0), (-1.0, 0), (0.7, 3), (1.0, 9)):
+        oj, _, _ = O.attention(*args, 32, jitter=scale, jitter_seed=seed)
+        diff = np.abs(oj - o).max(axis=1)
+        assert diff[det].max() <= 1e-3
+        moved_amb += int((diff[~det] > 0).sum())
+    assert moved_amb > 0
