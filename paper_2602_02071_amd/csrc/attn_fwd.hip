@@ -1,58 +1,112 @@
 // Fused BAPS attention forward (Alg. 1, the "E2E HiF8" workflow) for gfx950.
 //
-// One workgroup = 4 waves = 128 query rows of one key/value head: the rows
-// are the flattened (query position, query head of the group) pairs, so GQA
-// heads that share K/V share the workgroup, and batched decode (one query
-// position) packs its Hq/Hkv heads into one tile.  Each wave owns 32 rows.
+// Work split: a workgroup of NW waves owns 32*NW query rows of one key/value
+// head.  The rows are the flattened (query position, query head of the
+// group) pairs, so the Hq/Hkv query heads that share K/V share the
+// workgroup, and single-position decode packs its heads into one tile.  Each
+// wave owns 32 rows.
 //
-// Per key block j (the paper's key tile, processed in ascending order):
-//   - K_j and V_j are staged in LDS (V transposed, so that the key index is
-//     contiguous for the MFMA operand);
-//   - S^T = K_j Q^T on v_mfma_f32_32x32x16_bf16, fp32 accumulate.  In the
-//     S^T layout a lane holds 16 keys of one query per 32-key tile, so the
-//     row maximum is an in-lane max plus one exchange with lane^32;
-//   - the restart rule of Alg. 1 and the integer maximum of Sec. 3.3 run per
-//     query row (R8 per-row reading), with exact power-of-two rescales;
-//   - T = fl32(acc * c - ref) (eq. 3: the scale and the subtraction are one
-//     fused operation, rounded once), then P = HiF8(2^HiF8(T)) read from a
-//     table indexed by bits 31..19 of T (HiF8 rounding to nearest-away
-//     depends on those bits only);
-//   - the fp32 accumulator layout of S^T is directly the B operand layout of
-//     O^T = V_j^T P^T (the key order inside each 16-key group is permuted
-//     consistently on both operands), so P never leaves registers.
+// Per key block j (the paper's key tile, visited in ascending order):
+//   - K_j and V_j arrive in LDS through asynchronous global->LDS loads into a
+//     double buffer: the loads of block j+1 are in flight while block j is
+//     computed.  Both tiles keep their natural [key][d] layout with the
+//     16-byte chunks of each row XOR-swizzled, so that the MFMA operand reads
+//     below are free of bank conflicts;
+//   - S^T = K_j Q^T on v_mfma_f32_32x32x16_bf16 with fp32 accumulation (Q
+//     stays in registers).  In the S^T layout a lane holds 16 keys of one
+//     query per 32-key tile, so a row maximum is an in-lane max plus one
+//     exchange with lane^32;
+//   - block-aware precision rescaling per query row: the restart rule of
+//     Alg. 1 with threshold lambda, the integer running maximum of Sec. 3.3
+//     and exact power-of-two rescale factors;
+//   - T = fl32(acc * c - ref): the scale and the subtraction of eq. (3) are
+//     one fused multiply-add, rounded once; P = HiF8(2^HiF8(T)) is read from
+//     a 8192-entry LDS table indexed by bits 31..19 of T (HiF8 rounding to
+//     nearest-away depends on those bits only) and is exact in bf16;
+//   - the S^T accumulator layout is already the B operand layout of
+//     O^T += V_j^T P^T once the keys inside each 16-key group are taken in a
+//     fixed permuted order; the A operand (V^T fragments) comes straight from
+//     the [key][d] tile through ds_read_b64_tr_b16 transposing reads, in the
+//     same key order.  P never leaves registers.  The softmax of 32-key tile
+//     t+1 runs on the VALU while the PV MFMAs of tile t execute.
 #include "common.hpp"
 
 namespace baps {
 
 namespace {
 
-constexpr int kWaves = 4;
-constexpr int kThreads = 64 * kWaves;
 constexpr int kRowsPerWave = 32;
-constexpr int kTileRows = kWaves * kRowsPerWave;
 
-template <int D, int BLK>
-struct Smem {
-    static constexpr int kKStride = D + 8;       // u16 per K row in LDS (pad: 16 B)
-    static constexpr int kVStride = BLK + 8;     // u16 per V^T row in LDS
-    uint16_t k[BLK * kKStride];
-    uint16_t vt[D * kVStride];
-    uint16_t tab[kTabEntries];                   // P as bf16, indexed by T >> 19
-};
+typedef __bf16 bf16x2 __attribute__((__vector_size__(2 * sizeof(__bf16))));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+#define LDS_PTR(T, p) ((__attribute__((address_space(3))) T*)(p))
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
-template <int D, int BLK>
-__global__ __launch_bounds__(kThreads) void baps_attn_fwd_kernel(AttnParams p)
+// 16-byte chunk swizzles.  K: rows read 16 at a time at one logical chunk
+// (ds_read_b128).  V: rows read 4 at a time, two logical chunks (transposing
+// reads of 16 lanes).
+template <int D>
+__device__ __forceinline__ int k_swz(int r) { return D == 128 ? (r & 15) : ((r >> 1) & 7); }
+template <int D>
+__device__ __forceinline__ int v_swz(int r) { return D == 128 ? 2 * (r & 3) : 2 * ((r >> 1) & 1); }
+
+template <int D, int BLK, int NW>
+struct Cfg {
+    static constexpr int kThreads = 64 * NW;
+    static constexpr int kTileRows = kRowsPerWave * NW;
+    static constexpr int kRowBytes = 2 * D;
+    static constexpr int kCPR = D / 8;                       // 16-byte chunks per row
+    static constexpr int kTileBytes = BLK * kRowBytes;       // one K or V block
+    static constexpr int kLoadsPerTile = kTileBytes / 1024;  // 1 KiB per wave-wide load
+    static constexpr int kRowsPerLoad = 1024 / kRowBytes;
+    // dynamic LDS: [K0][V0][K1][V1]; the score table is a static LDS array
+    static constexpr int kLdsBytes = 4 * kTileBytes;
+};
+
+// One wave-wide asynchronous global->LDS load: lane l's 16 bytes at gptr land
+// at LDS byte lds_base + 16*l.  Issued as inline assembly so that the compiler
+// does not guard every later LDS read with a wait on these loads; the kernel
+// waits for them explicitly (vmcnt) before the barrier that publishes a tile.
+__device__ __forceinline__ void lds_dma_16(const void* gptr, uint32_t lds_base)
 {
-    static_assert(D % 32 == 0 && BLK % 32 == 0, "tile shape");
-    using SM = Smem<D, BLK>;
-    __shared__ __attribute__((aligned(16))) SM sm;
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+                 :
+                 : "v"(gptr), "s"(lds_base)
+                 : "memory", "m0");
+}
+
+// Issue the asynchronous loads of K (or V) rows [key0, key0 + BLK) into an
+// LDS tile; rows past the end re-read the last row (finite values that the
+// key mask removes).  Wave w issues loads w, w+NW, ...
+template <int D, int BLK, int NW, bool IS_V>
+__device__ __forceinline__ void load_tile(const uint16_t* base, int key0, int Sk, uint32_t lds_tile, int wave, int lane)
+{
+    using C = Cfg<D, BLK, NW>;
+#pragma unroll
+    for (int t = wave; t < C::kLoadsPerTile; t += NW) {
+        const int r = t * C::kRowsPerLoad + lane / C::kCPR;
+        const int p = lane % C::kCPR;
+        const int c = p ^ (IS_V ? v_swz<D>(r) : k_swz<D>(r));
+        const int key = min(key0 + r, Sk - 1);
+        const uint16_t* src = base + (long long)key * D + c * 8;
+        lds_dma_16(src, __builtin_amdgcn_readfirstlane(lds_tile + t * 1024));
+    }
+}
+
+template <int D, int BLK, int NW>
+__global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
+{
+    static_assert(D == 64 || D == 128, "head dimension");
+    static_assert(BLK % 32 == 0 && BLK <= 128, "key block");
+    using C = Cfg<D, BLK, NW>;
+    __shared__ __attribute__((aligned(16))) uint16_t tab[kTabEntries];
+    extern __shared__ __attribute__((aligned(1024))) char tiles[];
+    const uint32_t tiles_lds = (uint32_t)(uintptr_t)LDS_PTR(char, tiles);
 
     constexpr int kKT = BLK / 32;                 // 32-key tiles per block
     constexpr int kDK = D / 16;                   // 16-wide d chunks (QK^T contraction)
     constexpr int kDT = D / 32;                   // 32-wide d tiles of O^T
-    constexpr int kPC = BLK / 16;                 // 16-key chunks (PV contraction)
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -62,56 +116,49 @@ __global__ __launch_bounds__(kThreads) void baps_attn_fwd_kernel(AttnParams p)
 
     const int G = p.Hq / p.Hkv;
     const int flat_rows = p.Sq * G;
-    const int ntiles = (flat_rows + kTileRows - 1) / kTileRows;
-    const int tile = ntiles - 1 - (int)blockIdx.x;         // longest causal tiles first
+    const int ntiles = (flat_rows + C::kTileRows - 1) / C::kTileRows;
+    const int tile = ntiles - 1 - (int)blockIdx.x;          // longest causal tiles first
     const int g = blockIdx.y;
     const int b = blockIdx.z;
+    const uint16_t* kbase = p.k + ((long long)b * p.Hkv + g) * (long long)p.Sk * D;
+    const uint16_t* vbase = p.v + ((long long)b * p.Hkv + g) * (long long)p.Sk * D;
 
-    for (int i = tid; i < kTabEntries; i += kThreads) sm.tab[i] = (uint16_t)(p.tab[i] >> 16);
+    // key extent of the workgroup: its last row sees the most keys
+    const int off = p.Sk - p.Sq;                            // bottom-right causal alignment
+    const int f_last = min(flat_rows - 1, tile * C::kTileRows + C::kTileRows - 1);
+    const int kmax_tile = p.causal ? min(p.Sk - 1, f_last / G + off) : p.Sk - 1;
+    const int nblk = kmax_tile < 0 ? 0 : kmax_tile / BLK + 1;
+
+    if (nblk > 0) {
+        load_tile<D, BLK, NW, false>(kbase, 0, p.Sk, tiles_lds, wave, lane);
+        load_tile<D, BLK, NW, true>(vbase, 0, p.Sk, tiles_lds + C::kTileBytes, wave, lane);
+    }
+    for (int i = tid; i < kTabEntries; i += C::kThreads) tab[i] = (uint16_t)(p.tab[i] >> 16);
 
     // this lane's query row: flat index f = r * G + h_local
-    const int f = tile * kTileRows + wave * kRowsPerWave + j32;
+    const int f = tile * C::kTileRows + wave * kRowsPerWave + j32;
     const bool row_ok = f < flat_rows;
     const int r = row_ok ? f / G : 0;
     const int h = g * G + (row_ok ? f % G : 0);
-    const int off = p.Sk - p.Sq;                            // bottom-right causal alignment
-    const int kmax = p.causal ? min(p.Sk - 1, r + off) : p.Sk - 1;
-
-    // wave / workgroup extents of the key loop
-    int kmax_wave_hi = row_ok ? kmax : -1;
-    int kmax_wave_lo = row_ok ? kmax : 0x7fffffff;
+    const int kmax = row_ok ? (p.causal ? min(p.Sk - 1, r + off) : p.Sk - 1) : -1;
+    int kmax_wave_hi = kmax, kmax_wave_lo = row_ok ? kmax : 0x7fffffff;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
         kmax_wave_hi = max(kmax_wave_hi, __shfl_xor(kmax_wave_hi, o, 64));
         kmax_wave_lo = min(kmax_wave_lo, __shfl_xor(kmax_wave_lo, o, 64));
     }
-    int kmax_tile;
-    {
-        const int f_last = min(flat_rows - 1, tile * kTileRows + kTileRows - 1);
-        int kt_hi = -1;
-        // rows of a tile are consecutive positions; the largest position is the last row
-        const int r_last = f_last / G;
-        kt_hi = p.causal ? min(p.Sk - 1, r_last + off) : p.Sk - 1;
-        kmax_tile = kt_hi;
-    }
-    const int nblk = kmax_tile < 0 ? 0 : kmax_tile / BLK + 1;
 
     // Q^T as the B operand of S^T = K Q^T: lane holds Q[row][16*kk + 8*half .. +8]
     u32x4 qop[kDK];
     {
         const uint16_t* qrow = p.q + (((long long)b * p.Hq + h) * p.Sq + r) * D;
 #pragma unroll
-        for (int kk = 0; kk < kDK; ++kk) {
-            if (row_ok) qop[kk] = *reinterpret_cast<const u32x4*>(qrow + kk * 16 + half * 8);
-            else qop[kk] = u32x4{0, 0, 0, 0};
-        }
+        for (int kk = 0; kk < kDK; ++kk)
+            qop[kk] = row_ok ? *reinterpret_cast<const u32x4*>(qrow + kk * 16 + half * 8) : u32x4{0, 0, 0, 0};
     }
 
-    const uint16_t* kbase = p.k + ((long long)b * p.Hkv + g) * (long long)p.Sk * D;
-    const uint16_t* vbase = p.v + ((long long)b * p.Hkv + g) * (long long)p.Sk * D;
     const float ninf = -__builtin_huge_valf();
     const float c = p.c;
-
     float m = ninf;                 // running integer maximum of this lane's row
     float dl = 0.0f;                // this lane's share of the denominator
     unsigned n_restart = 0, n_visit = 0;
@@ -119,26 +166,23 @@ __global__ __launch_bounds__(kThreads) void baps_attn_fwd_kernel(AttnParams p)
 #pragma unroll
     for (int t = 0; t < kDT; ++t) oacc[t] = f32x16{};
 
+    // per-lane parts of the LDS addresses
+    const int k_row_lo = j32;                                // K operand: row kt*32 + j32
+    const int tr_s = lane & 15;                              // V transposing reads
+    const int tr_row = 4 * half + tr_s / 4;                  // + 16*pc (+ 8 for slots 4..7)
+    const int tr_d = 16 * ((lane >> 4) & 1) + 4 * (tr_s & 3);   // + 32*dt
+
     for (int jb = 0; jb < nblk; ++jb) {
         const int key0 = jb * BLK;
-        __syncthreads();                                    // previous block's LDS reads done
-        // stage K_j row-major and V_j transposed; rows past Sk are zeros
-        for (int i = tid; i < BLK * (D / 8); i += kThreads) {
-            const int kr = i / (D / 8);
-            const int d8 = i % (D / 8);
-            u32x4 kv = {0, 0, 0, 0}, vv = {0, 0, 0, 0};
-            if (key0 + kr < p.Sk) {
-                kv = *reinterpret_cast<const u32x4*>(kbase + (long long)(key0 + kr) * D + d8 * 8);
-                vv = *reinterpret_cast<const u32x4*>(vbase + (long long)(key0 + kr) * D + d8 * 8);
-            }
-            *reinterpret_cast<u32x4*>(&sm.k[kr * SM::kKStride + d8 * 8]) = kv;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                sm.vt[(d8 * 8 + 2 * e) * SM::kVStride + kr] = (uint16_t)(vv[e] & 0xffffu);
-                sm.vt[(d8 * 8 + 2 * e + 1) * SM::kVStride + kr] = (uint16_t)(vv[e] >> 16);
-            }
+        const char* kt_lds = tiles + (jb & 1) * 2 * C::kTileBytes;
+        const char* vt_lds = kt_lds + C::kTileBytes;
+        __builtin_amdgcn_s_waitcnt(0);                      // this wave's loads of block jb landed
+        __syncthreads();                                    // everyone's did; block jb-1 fully consumed
+        if (jb + 1 < nblk) {
+            const uint32_t nk = tiles_lds + ((jb + 1) & 1) * 2 * C::kTileBytes;
+            load_tile<D, BLK, NW, false>(kbase, key0 + BLK, p.Sk, nk, wave, lane);
+            load_tile<D, BLK, NW, true>(vbase, key0 + BLK, p.Sk, nk + C::kTileBytes, wave, lane);
         }
-        __syncthreads();
         if (key0 > kmax_wave_hi) continue;                  // nothing visible for this wave
 
         // S^T = K_j Q^T
@@ -146,12 +190,12 @@ __global__ __launch_bounds__(kThreads) void baps_attn_fwd_kernel(AttnParams p)
 #pragma unroll
         for (int kt = 0; kt < kKT; ++kt) {
             sacc[kt] = f32x16{};
+            const int row = kt * 32 + k_row_lo;
 #pragma unroll
             for (int kk = 0; kk < kDK; ++kk) {
-                const u32x4 a = *reinterpret_cast<const u32x4*>(
-                    &sm.k[(kt * 32 + j32) * SM::kKStride + kk * 16 + half * 8]);
-                sacc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(qop[kk]),
-                                                                    sacc[kt], 0, 0, 0);
+                const int chunk = (2 * kk + half) ^ k_swz<D>(row);
+                const u32x4 a = *reinterpret_cast<const u32x4*>(kt_lds + row * C::kRowBytes + chunk * 16);
+                sacc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(qop[kk]), sacc[kt], 0, 0, 0);
             }
         }
         // mask keys past kmax (causal diagonal, ragged tail); key of register
@@ -170,11 +214,11 @@ __global__ __launch_bounds__(kThreads) void baps_attn_fwd_kernel(AttnParams p)
 #pragma unroll
         for (int kt = 0; kt < kKT; ++kt)
 #pragma unroll
-            for (int i = 0; i < 16; ++i) amax = fmaxf(amax, sacc[kt][i]);
+            for (int i = 0; i < 16; i += 2) amax = fmaxf(amax, fmaxf(sacc[kt][i], sacc[kt][i + 1]));
         amax = fmaxf(amax, __shfl_xor(amax, 32, 64));
 
         // block-aware precision rescaling (Alg. 1), per row
-        float ref, ab, beta;                 // ab = alpha / beta, exact powers of two
+        float ref, ab, beta;                 // ab = alpha / beta; all exact powers of two
         if (amax == ninf) {                  // no visible key in this block: no-op
             ref = 0.0f; ab = 1.0f; beta = 1.0f;
         } else {
@@ -200,52 +244,54 @@ __global__ __launch_bounds__(kThreads) void baps_attn_fwd_kernel(AttnParams p)
             beta = exp2_int(ref - m_new);
             m = m_new;
         }
-
-        // P = HiF8(2^HiF8(T)), T = fl32(acc * c - ref); packed as bf16 B operands
-        u32x4 pop[kPC];
-        float rs = 0.0f;
-#pragma unroll
-        for (int kt = 0; kt < kKT; ++kt) {
-#pragma unroll
-            for (int ch = 0; ch < 2; ++ch) {
-                uint32_t w[4];
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const float t0 = __builtin_fmaf(sacc[kt][ch * 8 + 2 * e], c, -ref);
-                    const float t1 = __builtin_fmaf(sacc[kt][ch * 8 + 2 * e + 1], c, -ref);
-                    const uint32_t p0 = sm.tab[hif8::f2u(t0) >> kTabShift];
-                    const uint32_t p1 = sm.tab[hif8::f2u(t1) >> kTabShift];
-                    rs += hif8::u2f(p0 << 16);
-                    rs += hif8::u2f(p1 << 16);
-                    w[e] = p0 | (p1 << 16);
-                }
-                pop[kt * 2 + ch] = u32x4{w[0], w[1], w[2], w[3]};
-            }
-        }
-
-        // d = alpha d + beta rowsum and O~ = alpha O~ + beta P V, written as
-        // beta * ((alpha/beta) X + Y): identical in fp32, powers of two are exact
+        // d = alpha d + beta rowsum and O~ = alpha O~ + beta P V, evaluated as
+        // beta * ((alpha/beta) X + Y): identical in fp32, the factors are powers of two
         if (__any(ab != 1.0f)) {
 #pragma unroll
             for (int t = 0; t < kDT; ++t)
 #pragma unroll
                 for (int i = 0; i < 16; ++i) oacc[t][i] *= ab;
         }
-        dl = dl * ab + rs;
+        dl *= ab;
 
-        // O~^T += V_j^T P^T; A operand: lane holds V^T[d][keys] for the same
-        // permuted 16-key order as the B operand taken from the S^T layout
+        const float nref = -ref;
+        const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 #pragma unroll
-        for (int pc = 0; pc < kPC; ++pc) {
-            const int kb0 = pc * 16 + 4 * half;
+        for (int kt = 0; kt < kKT; ++kt) {
+            // P = HiF8(2^HiF8(T)) for this 32-key tile, packed as two bf16 B operands
+            u32x4 pop[2];
 #pragma unroll
-            for (int t = 0; t < kDT; ++t) {
-                const uint16_t* vr = &sm.vt[(t * 32 + j32) * SM::kVStride];
-                const u32x2 lo = *reinterpret_cast<const u32x2*>(vr + kb0);
-                const u32x2 hi = *reinterpret_cast<const u32x2*>(vr + kb0 + 8);
-                const u32x4 a = {lo[0], lo[1], hi[0], hi[1]};
-                oacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(pop[pc]),
-                                                                   oacc[t], 0, 0, 0);
+            for (int ch = 0; ch < 2; ++ch) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float t0 = __builtin_fmaf(sacc[kt][ch * 8 + 2 * e], c, nref);
+                    const float t1 = __builtin_fmaf(sacc[kt][ch * 8 + 2 * e + 1], c, nref);
+                    const uint32_t p0 = tab[hif8::f2u(t0) >> kTabShift];
+                    const uint32_t p1 = tab[hif8::f2u(t1) >> kTabShift];
+                    const uint32_t w = p0 | (p1 << 16);
+                    pop[ch][e] = w;
+                    dl = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), ones, dl, false);
+                }
+            }
+            // O~^T += V_j^T P^T over this tile's two 16-key chunks
+#pragma unroll
+            for (int ch = 0; ch < 2; ++ch) {
+                const int pc = 2 * kt + ch;
+#pragma unroll
+                for (int t = 0; t < kDT; ++t) {
+                    const int d = 32 * t + tr_d;
+                    const int row_a = 16 * pc + tr_row;
+                    const int row_b = row_a + 8;
+                    const int ca = (d >> 3) ^ v_swz<D>(row_a);
+                    const int cb = (d >> 3) ^ v_swz<D>(row_b);
+                    const char* pa = vt_lds + row_a * C::kRowBytes + ca * 16 + (d & 7) * 2;
+                    const char* pb = vt_lds + row_b * C::kRowBytes + cb * 16 + (d & 7) * 2;
+                    const s16x4 va = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LDS_PTR(s16x4, pa));
+                    const s16x4 vb = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LDS_PTR(s16x4, pb));
+                    const u32x4 a = {__builtin_bit_cast(u32x2, va)[0], __builtin_bit_cast(u32x2, va)[1],
+                                     __builtin_bit_cast(u32x2, vb)[0], __builtin_bit_cast(u32x2, vb)[1]};
+                    oacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(pop[ch]), oacc[t], 0, 0, 0);
+                }
             }
         }
         if (__any(beta != 1.0f)) {
@@ -280,26 +326,42 @@ __global__ __launch_bounds__(kThreads) void baps_attn_fwd_kernel(AttnParams p)
     }
 }
 
-template <int D, int BLK>
+template <int D, int BLK, int NW>
 hipError_t launch_one(const AttnParams& p, hipStream_t st)
 {
-    const int G = p.Hq / p.Hkv;
-    const long long flat = (long long)p.Sq * G;
-    const dim3 grid((unsigned)((flat + kTileRows - 1) / kTileRows), (unsigned)p.Hkv, (unsigned)p.B);
-    hipLaunchKernelGGL((baps_attn_fwd_kernel<D, BLK>), grid, dim3(kThreads), 0, st, p);
+    using C = Cfg<D, BLK, NW>;
+    static bool attr_set = false;
+    if (!attr_set) {
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&baps_attn_fwd_kernel<D, BLK, NW>),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, C::kLdsBytes);
+        if (e != hipSuccess) return e;
+        attr_set = true;
+    }
+    const long long flat = (long long)p.Sq * (p.Hq / p.Hkv);
+    const dim3 grid((unsigned)((flat + C::kTileRows - 1) / C::kTileRows), (unsigned)p.Hkv, (unsigned)p.B);
+    hipLaunchKernelGGL((baps_attn_fwd_kernel<D, BLK, NW>), grid, dim3(C::kThreads), C::kLdsBytes, st, p);
     return hipGetLastError();
+}
+
+template <int D, int BLK>
+hipError_t launch_d_blk(const AttnParams& p, hipStream_t st)
+{
+    // few rows per key/value head (decode, short queries): one wave per workgroup
+    const long long flat = (long long)p.Sq * (p.Hq / p.Hkv);
+    if (flat <= 64) return launch_one<D, BLK, 1>(p, st);
+    return launch_one<D, BLK, 8>(p, st);
 }
 
 }  // namespace
 
 hipError_t launch_attention(const AttnParams& p, int D, int block, hipStream_t st)
 {
-    if (D == 64 && block == 64) return launch_one<64, 64>(p, st);
-    if (D == 64 && block == 128) return launch_one<64, 128>(p, st);
-    if (D == 128 && block == 64) return launch_one<128, 64>(p, st);
-    if (D == 128 && block == 128) return launch_one<128, 128>(p, st);
-    if (D == 64 && block == 32) return launch_one<64, 32>(p, st);
-    if (D == 128 && block == 32) return launch_one<128, 32>(p, st);
+    if (D == 64 && block == 32) return launch_d_blk<64, 32>(p, st);
+    if (D == 64 && block == 64) return launch_d_blk<64, 64>(p, st);
+    if (D == 64 && block == 128) return launch_d_blk<64, 128>(p, st);
+    if (D == 128 && block == 32) return launch_d_blk<128, 32>(p, st);
+    if (D == 128 && block == 64) return launch_d_blk<128, 64>(p, st);
+    if (D == 128 && block == 128) return launch_d_blk<128, 128>(p, st);
     return hipErrorInvalidValue;
 }
 
