@@ -113,6 +113,8 @@ def main():
     ap.add_argument("--config", type=int, default=2, help="workload 1..5 (2 = Llama-3-8B prefill)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="also run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
@@ -155,6 +157,15 @@ def main():
                          "traffic": _traffic("attn_fwd_decode")}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, qkv)
+    if args.calib_copy_mib:
+        import torch
+        n = args.calib_copy_mib << 20
+        src = torch.ones(n // 4, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        out["calib_copy_bytes"] = n
     print(json.dumps(out), flush=True)
 
 

@@ -110,7 +110,7 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int j32 = lane & 31;
     const int half = lane >> 5;
 
@@ -147,6 +147,9 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
         kmax_wave_hi = max(kmax_wave_hi, __shfl_xor(kmax_wave_hi, o, 64));
         kmax_wave_lo = min(kmax_wave_lo, __shfl_xor(kmax_wave_lo, o, 64));
     }
+    // wave-uniform from here on: keeps the skip and mask branches scalar
+    kmax_wave_hi = __builtin_amdgcn_readfirstlane(kmax_wave_hi);
+    kmax_wave_lo = __builtin_amdgcn_readfirstlane(kmax_wave_lo);
 
     // Q^T as the B operand of S^T = K Q^T: lane holds Q[row][16*kk + 8*half .. +8]
     u32x4 qop[kDK];
@@ -159,18 +162,43 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
 
     const float ninf = -__builtin_huge_valf();
     const float c = p.c;
-    float m = ninf;                 // running integer maximum of this lane's row
-    float dl = 0.0f;                // this lane's share of the denominator
+    const float lam = (float)p.lambda;
+    // Alg. 1 state of this lane's row.  The output and the denominator are
+    // kept relative to the current block reference ref_j instead of the
+    // running maximum m_j: X_j = sum_{i<=j} 2^(ref_i - ref_j) P_i V_i and
+    // dX_j likewise, so O~_j = 2^(ref_j - m_j) X_j and d_j = 2^(ref_j - m_j) dX_j.
+    // The two power-of-two rescales of a block (2^(m_{j-1}-m_j) on the old
+    // state, 2^(ref_j - m_j) on the new block) fold into one exact rescale by
+    // 2^(ref_{j-1} - ref_j), needed only when the reference moves, and the
+    // normalisation O = O~/d = X/dX is unchanged.
+    float m = ninf;                 // running integer maximum m_j
+    float ref = ninf;               // current block reference
+    float dl = 0.0f;                // this lane's share of dX
     unsigned n_restart = 0, n_visit = 0;
     f32x16 oacc[kDT];
 #pragma unroll
     for (int t = 0; t < kDT; ++t) oacc[t] = f32x16{};
 
-    // per-lane parts of the LDS addresses
-    const int k_row_lo = j32;                                // K operand: row kt*32 + j32
-    const int tr_s = lane & 15;                              // V transposing reads
-    const int tr_row = 4 * half + tr_s / 4;                  // + 16*pc (+ 8 for slots 4..7)
-    const int tr_d = 16 * ((lane >> 4) & 1) + 4 * (tr_s & 3);   // + 32*dt
+    // per-lane LDS byte offsets of the operand reads inside a tile
+    uint32_t koff[kDK];
+    {
+        const int kx = k_swz<D>(j32);            // swizzle of row kt*32 + j32 depends on j32 only
+#pragma unroll
+        for (int kk = 0; kk < kDK; ++kk) koff[kk] = j32 * C::kRowBytes + 16 * ((2 * kk + half) ^ kx);
+    }
+    uint32_t voff[kDT];
+    {
+        // transposing reads: lane l of a 16-lane group points at row
+        // 16*pc + 4*half + (l%16)/4 (+8 for slots 4..7) and at 4 values of d
+        const int s16 = lane & 15;
+        const int row0 = 4 * half + s16 / 4;
+        const int vx = v_swz<D>(row0);          // invariant under +16*pc and +8
+#pragma unroll
+        for (int t = 0; t < kDT; ++t) {
+            const int d = 32 * t + 16 * ((lane >> 4) & 1) + 4 * (s16 & 3);
+            voff[t] = row0 * C::kRowBytes + 16 * ((d >> 3) ^ vx) + 2 * (d & 7);
+        }
+    }
 
     for (int jb = 0; jb < nblk; ++jb) {
         const int key0 = jb * BLK;
@@ -185,80 +213,76 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
         }
         if (key0 > kmax_wave_hi) continue;                  // nothing visible for this wave
 
-        // S^T = K_j Q^T
+        // S^T = K_j Q^T.  The wave raises its priority for the MFMA burst so
+        // that the two waves sharing a SIMD drift apart: one runs its QK^T
+        // MFMAs while the other runs the VALU softmax of its block.
+        __builtin_amdgcn_s_setprio(2);
         f32x16 sacc[kKT];
 #pragma unroll
-        for (int kt = 0; kt < kKT; ++kt) {
-            sacc[kt] = f32x16{};
-            const int row = kt * 32 + k_row_lo;
+        for (int kt = 0; kt < kKT; ++kt) sacc[kt] = f32x16{};
 #pragma unroll
-            for (int kk = 0; kk < kDK; ++kk) {
-                const int chunk = (2 * kk + half) ^ k_swz<D>(row);
-                const u32x4 a = *reinterpret_cast<const u32x4*>(kt_lds + row * C::kRowBytes + chunk * 16);
+        for (int kk = 0; kk < kDK; ++kk) {
+            const char* kp = kt_lds + koff[kk];
+#pragma unroll
+            for (int kt = 0; kt < kKT; ++kt) {
+                const u32x4 a = *reinterpret_cast<const u32x4*>(kp + kt * 32 * C::kRowBytes);
                 sacc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(qop[kk]), sacc[kt], 0, 0, 0);
             }
         }
+        __builtin_amdgcn_s_setprio(0);
         // mask keys past kmax (causal diagonal, ragged tail); key of register
         // i of tile kt: key0 + 32*kt + 8*(i/4) + 4*half + i%4
         if (key0 + BLK - 1 > kmax_wave_lo) {
+            asm volatile("" ::: "memory");          // keep this a real branch (no if-conversion)
+            const int lim = kmax - key0 - 4 * half;
 #pragma unroll
             for (int kt = 0; kt < kKT; ++kt)
 #pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int key = key0 + kt * 32 + 8 * (i / 4) + 4 * half + (i % 4);
-                    if (key > kmax) sacc[kt][i] = ninf;
-                }
+                for (int i = 0; i < 16; ++i)
+                    if (kt * 32 + 8 * (i / 4) + (i % 4) > lim) sacc[kt][i] = ninf;
         }
         // row maximum of the raw dot products (the scale c > 0 is monotone)
         float amax = ninf;
 #pragma unroll
         for (int kt = 0; kt < kKT; ++kt)
 #pragma unroll
-            for (int i = 0; i < 16; i += 2) amax = fmaxf(amax, fmaxf(sacc[kt][i], sacc[kt][i + 1]));
-        amax = fmaxf(amax, __shfl_xor(amax, 32, 64));
+            for (int i = 0; i < 16; i += 2) amax = __builtin_fmaxf(amax, __builtin_fmaxf(sacc[kt][i], sacc[kt][i + 1]));
+        amax = __builtin_fmaxf(amax, __shfl_xor(amax, 32, 64));
 
-        // block-aware precision rescaling (Alg. 1), per row
-        float ref, ab, beta;                 // ab = alpha / beta; all exact powers of two
-        if (amax == ninf) {                  // no visible key in this block: no-op
-            ref = 0.0f; ab = 1.0f; beta = 1.0f;
-        } else {
-            bool restart;
-            float tq = 0.0f;
-            if (jb < p.n_b0 || m == ninf) {
-                restart = true;
-            } else {
-                tq = hif8::round(__builtin_fmaf(amax, c, -m));   // rowmax of the 8-bit T
-                restart = ceilf(tq) > (float)p.lambda;
-                ++n_visit;
-                n_restart += restart ? 1u : 0u;
-            }
-            float m_new;
-            if (restart) {
-                m_new = fmaxf(m, ceilf(amax * c));               // ceil(rowmax S), S in fp32
-                ref = m_new;
-            } else {
-                m_new = m + fmaxf(0.0f, ceilf(tq));
-                ref = m;
-            }
-            ab = (m == ninf) ? 0.0f : exp2_int(m - ref);
-            beta = exp2_int(ref - m_new);
-            m = m_new;
-        }
-        // d = alpha d + beta rowsum and O~ = alpha O~ + beta P V, evaluated as
-        // beta * ((alpha/beta) X + Y): identical in fp32, the factors are powers of two
-        if (__any(ab != 1.0f)) {
+        // block-aware precision rescaling (Alg. 1), per row, branch-free.
+        // B0 blocks (and a first block with m = -inf) take the high-precision
+        // path; B1 blocks restart when ceil(rowmax T) > lambda, where rowmax of
+        // the 8-bit T = fl32(acc*c - m) is the 8-bit cast of the raw maximum's
+        // T (the cast is monotone).
+        const bool vis = amax != ninf;
+        const bool forced = (jb < p.n_b0) || (m == ninf);
+        const float tq = hif8::round(__builtin_fmaf(amax, c, -m));
+        const bool restart = forced || (ceilf(tq) > lam);
+        const float m_hi = __builtin_fmaxf(m, ceilf(amax * c));    // ceil(rowmax S), S in fp32
+        const float m_new = vis ? (restart ? m_hi : m + __builtin_fmaxf(0.0f, ceilf(tq))) : m;
+        const float ref_new = vis ? (restart ? m_hi : m) : ref;
+        const bool b1 = vis && (jb >= p.n_b0);
+        n_visit += b1 ? 1u : 0u;
+        n_restart += (b1 && restart) ? 1u : 0u;
+        const float f = (ref == ninf) ? 1.0f : exp2_int(ref - ref_new);
+        if (__any(f != 1.0f)) {
 #pragma unroll
             for (int t = 0; t < kDT; ++t)
 #pragma unroll
-                for (int i = 0; i < 16; ++i) oacc[t][i] *= ab;
+                for (int i = 0; i < 16; ++i) oacc[t][i] *= f;
         }
-        dl *= ab;
+        dl *= f;
+        m = m_new;
+        ref = ref_new;
 
-        const float nref = -ref;
+        // a row with no visible key so far keeps ref = -inf; its masked scores
+        // (acc = -inf) must still give T = -inf and P = 0
+        const float nref = (ref == ninf) ? 0.0f : -ref;
         const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 #pragma unroll
         for (int kt = 0; kt < kKT; ++kt) {
-            // P = HiF8(2^HiF8(T)) for this 32-key tile, packed as two bf16 B operands
+            // P = HiF8(2^HiF8(T)), T = fl32(acc*c - ref), for this 32-key tile,
+            // packed as two bf16 B operands
             u32x4 pop[2];
 #pragma unroll
             for (int ch = 0; ch < 2; ++ch) {
@@ -273,52 +297,40 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
                     dl = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), ones, dl, false);
                 }
             }
-            // O~^T += V_j^T P^T over this tile's two 16-key chunks
+            // X^T += V_j^T P^T over this tile's two 16-key chunks
 #pragma unroll
             for (int ch = 0; ch < 2; ++ch) {
                 const int pc = 2 * kt + ch;
 #pragma unroll
                 for (int t = 0; t < kDT; ++t) {
-                    const int d = 32 * t + tr_d;
-                    const int row_a = 16 * pc + tr_row;
-                    const int row_b = row_a + 8;
-                    const int ca = (d >> 3) ^ v_swz<D>(row_a);
-                    const int cb = (d >> 3) ^ v_swz<D>(row_b);
-                    const char* pa = vt_lds + row_a * C::kRowBytes + ca * 16 + (d & 7) * 2;
-                    const char* pb = vt_lds + row_b * C::kRowBytes + cb * 16 + (d & 7) * 2;
+                    const char* pa = vt_lds + voff[t] + pc * 16 * C::kRowBytes;
                     const s16x4 va = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LDS_PTR(s16x4, pa));
-                    const s16x4 vb = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LDS_PTR(s16x4, pb));
+                    const s16x4 vb = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LDS_PTR(s16x4, pa + 8 * C::kRowBytes));
                     const u32x4 a = {__builtin_bit_cast(u32x2, va)[0], __builtin_bit_cast(u32x2, va)[1],
                                      __builtin_bit_cast(u32x2, vb)[0], __builtin_bit_cast(u32x2, vb)[1]};
                     oacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(pop[ch]), oacc[t], 0, 0, 0);
                 }
             }
         }
-        if (__any(beta != 1.0f)) {
-#pragma unroll
-            for (int t = 0; t < kDT; ++t)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) oacc[t][i] *= beta;
-        }
-        dl *= beta;
     }
 
-    // epilogue: O = diag(d)^-1 O~, lse = ln2 (m + log2 d)
+    // epilogue: O = X / dX, lse = ln2 (ref + log2 dX) = ln2 (m + log2 d)
     const float d = dl + __shfl_xor(dl, 32, 64);
     if (!row_ok) return;
     float* orow = p.o + (((long long)b * p.Hq + h) * p.Sq + r) * D;
-    const bool empty = (m == ninf);
+    const bool empty = (ref == ninf);
+    const float inv = empty ? 0.0f : 1.0f / d;
 #pragma unroll
     for (int t = 0; t < kDT; ++t)
 #pragma unroll
         for (int q4 = 0; q4 < 4; ++q4) {
             f32x4 v;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = empty ? 0.0f : oacc[t][q4 * 4 + e] / d;
+            for (int e = 0; e < 4; ++e) v[e] = oacc[t][q4 * 4 + e] * inv;
             *reinterpret_cast<f32x4*>(orow + t * 32 + q4 * 8 + half * 4) = v;
         }
     if (half == 0) {
-        if (p.lse) p.lse[((long long)b * p.Hq + h) * p.Sq + r] = empty ? ninf : 0.69314718055994531f * (m + log2f(d));
+        if (p.lse) p.lse[((long long)b * p.Hq + h) * p.Sq + r] = empty ? ninf : 0.69314718055994531f * (ref + log2f(d));
         if (p.counters && n_visit) {
             atomicAdd(p.counters + 2 * ((long long)b * p.Hq + h) + 0, (unsigned long long)n_restart);
             atomicAdd(p.counters + 2 * ((long long)b * p.Hq + h) + 1, (unsigned long long)n_visit);
