@@ -1,0 +1,318 @@
+// Fused BAPS attention forward for few query rows per key/value head
+// (batched decode, speculative or chunked short queries).  Same method and
+// state machine as the prefill kernel (Alg. 1 per query row, block-aware
+// rescaling, HiF8 T and P), shaped for the HBM-bound regime:
+//
+//   - one wave per workgroup owns up to 16 flattened (query position, query
+//     head of the group) rows of one key/value head, on 16x16x32 bf16 MFMAs;
+//   - K and V stream through a ring of LDS slots of 32 keys each, filled by
+//     asynchronous global->LDS loads kept R slots ahead.  A single wave needs
+//     no barrier: each slot is consumed after the vector-memory counter says
+//     its loads landed, and refilled after the MFMAs that read it were issued;
+//   - 80 KiB of LDS per workgroup (ring + score table), so two workgroups
+//     share a CU and every (batch, key/value head) stream of a large batch
+//     is in flight at once.
+#include "common.hpp"
+
+namespace baps {
+
+namespace {
+
+typedef __bf16 bf16x2 __attribute__((__vector_size__(2 * sizeof(__bf16))));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+#define LDS_PTR(T, p) ((__attribute__((address_space(3))) T*)(p))
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+constexpr int kRows = 16;            // query rows per workgroup
+constexpr int kSlotKeys = 32;        // keys per ring slot
+
+template <int D>
+struct DCfg {
+    static constexpr int kRowBytes = 2 * D;
+    static constexpr int kCPR = D / 8;                          // 16-byte chunks per row
+    static constexpr int kSlotBytes = kSlotKeys * kRowBytes;    // 8 KiB (D=128), 4 KiB (D=64)
+    static constexpr int kIPS = kSlotBytes / 1024;              // wave-wide loads per slot
+    static constexpr int kRing = 64 / kIPS;                     // slots; keeps <= 63 loads outstanding
+    static constexpr int kLdsBytes = kRing * kSlotBytes;
+};
+
+// chunk swizzles (same bank-conflict reasoning as the prefill kernel): K rows
+// are read 16 at a time at one logical chunk, V rows 4 at a time, 2 chunks
+template <int D>
+__device__ __forceinline__ int k_swz(int r) { return D == 128 ? (r & 15) : ((r >> 1) & 7); }
+template <int D>
+__device__ __forceinline__ int v_swz(int r) { return D == 128 ? 2 * (r & 3) : 2 * ((r >> 1) & 1); }
+
+__device__ __forceinline__ void lds_dma_16(const void* gptr, uint32_t lds_base)
+{
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+                 :
+                 : "v"(gptr), "s"(lds_base)
+                 : "memory", "m0");
+}
+
+// wait until at most n wave-wide loads of this wave are outstanding
+__device__ __forceinline__ void wait_vm(int n)
+{
+    switch (n) {
+#define W(N) case N: __builtin_amdgcn_s_waitcnt(0xF70 | ((N) & 15) | ((((N) >> 4) & 3) << 14)); break;
+        W(0) W(4) W(8) W(12) W(16) W(20) W(24) W(28) W(32) W(36) W(40) W(44) W(48) W(52) W(56) W(60)
+#undef W
+    default: __builtin_amdgcn_s_waitcnt(0xF70); break;
+    }
+}
+
+template <int D, int BLK>
+__global__ __launch_bounds__(64) void baps_attn_decode_kernel(AttnParams p)
+{
+    static_assert(D == 64 || D == 128, "head dimension");
+    static_assert(BLK % kSlotKeys == 0 && BLK <= 128, "key block");
+    using C = DCfg<D>;
+    __shared__ __attribute__((aligned(16))) uint16_t tab[kTabEntries];
+    extern __shared__ __attribute__((aligned(1024))) char ring[];
+    const uint32_t ring_lds = (uint32_t)(uintptr_t)LDS_PTR(char, ring);
+
+    constexpr int kSPB = BLK / kSlotKeys;        // K (and V) slots per block
+    constexpr int kKT = BLK / 16;                 // 16-key S^T tiles per block
+    constexpr int kDK = D / 32;                   // 32-wide d chunks (QK^T contraction)
+    constexpr int kDT = D / 16;                   // 16-wide d tiles of O^T
+
+    const int lane = threadIdx.x;
+    const int c16 = lane & 15;                    // query column of this lane
+    const int grp = lane >> 4;                    // lane group 0..3
+
+    const int G = p.Hq / p.Hkv;
+    const int flat_rows = p.Sq * G;
+    const int tile = blockIdx.x;
+    const int g = blockIdx.y;
+    const int b = blockIdx.z;
+    const uint16_t* kbase = p.k + ((long long)b * p.Hkv + g) * (long long)p.Sk * D;
+    const uint16_t* vbase = p.v + ((long long)b * p.Hkv + g) * (long long)p.Sk * D;
+
+    const int off = p.Sk - p.Sq;
+    const int f_last = min(flat_rows - 1, tile * kRows + kRows - 1);
+    const int kmax_tile = p.causal ? min(p.Sk - 1, f_last / G + off) : p.Sk - 1;
+    const int nblk = kmax_tile < 0 ? 0 : kmax_tile / BLK + 1;
+    const int nslots = 2 * kSPB * nblk;           // K slots then V slots, block by block
+
+    // slot n: block n / (2 kSPB); within the block K slots first, then V
+    auto issue_slot = [&](int n) {
+        const int jb = n / (2 * kSPB);
+        const int w = n % (2 * kSPB);
+        const bool is_v = w >= kSPB;
+        const int key0 = jb * BLK + (w % kSPB) * kSlotKeys;
+        const uint16_t* base = is_v ? vbase : kbase;
+        const uint32_t dst = ring_lds + (uint32_t)((n % C::kRing) * C::kSlotBytes);
+#pragma unroll
+        for (int t = 0; t < C::kIPS; ++t) {
+            const int r = t * (1024 / C::kRowBytes) + lane / C::kCPR;
+            const int pch = lane % C::kCPR;
+            const int ch = pch ^ (is_v ? v_swz<D>(r) : k_swz<D>(r));
+            const int key = min(key0 + r, p.Sk - 1);
+            lds_dma_16(base + (long long)key * D + ch * 8, dst + t * 1024);
+        }
+    };
+    int issued = 0;
+    for (; issued < min(nslots, C::kRing); ++issued) issue_slot(issued);
+
+    for (int i = lane; i < kTabEntries; i += 64) tab[i] = (uint16_t)(p.tab[i] >> 16);
+
+    // this lane's query row
+    const int f = tile * kRows + c16;
+    const bool row_ok = f < flat_rows;
+    const int r = row_ok ? f / G : 0;
+    const int h = g * G + (row_ok ? f % G : 0);
+    const int kmax = row_ok ? (p.causal ? min(p.Sk - 1, r + off) : p.Sk - 1) : -1;
+    int kmax_lo = row_ok ? kmax : 0x7fffffff;
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) kmax_lo = min(kmax_lo, __shfl_xor(kmax_lo, o, 64));
+    kmax_lo = __builtin_amdgcn_readfirstlane(kmax_lo);
+
+    // Q^T as the B operand of S^T = K Q^T (16x16x32): lane holds
+    // Q[row][32*kk + 8*grp .. +8]; K uses the same d order
+    u32x4 qop[kDK];
+    {
+        const uint16_t* qrow = p.q + (((long long)b * p.Hq + h) * p.Sq + r) * D;
+#pragma unroll
+        for (int kk = 0; kk < kDK; ++kk)
+            qop[kk] = row_ok ? *reinterpret_cast<const u32x4*>(qrow + kk * 32 + grp * 8) : u32x4{0, 0, 0, 0};
+    }
+
+    const float ninf = -__builtin_huge_valf();
+    const float c = p.c;
+    const float lam = (float)p.lambda;
+    // Alg. 1 state; output and denominator kept relative to the current
+    // block reference (one exact rescale when the reference moves)
+    float m = ninf, ref = ninf, dl = 0.0f;
+    unsigned n_restart = 0, n_visit = 0;
+    f32x4 oacc[kDT];
+#pragma unroll
+    for (int t = 0; t < kDT; ++t) oacc[t] = f32x4{};
+
+    const int kx = k_swz<D>(c16);                 // K rows 16*kt + c16
+    const uint32_t krow = c16 * C::kRowBytes;
+    const int vrow0 = 4 * grp + c16 / 4;          // + 32*slot row offsets, +16 for slots 4..7
+    const int vx = v_swz<D>(vrow0);
+    const int vd0 = 4 * (c16 & 3);                // + 16*dt
+    const uint32_t vrow = vrow0 * C::kRowBytes + 2 * (vd0 & 7);
+
+    int consumed = 0;
+    auto wait_slot = [&](int n) {                 // slot n has landed in LDS
+        wait_vm((issued - 1 - n) * C::kIPS);
+    };
+    auto next_slot = [&]() {                      // the slot just read is refilled
+        if (issued < nslots) { issue_slot(issued); ++issued; }
+        ++consumed;
+    };
+
+    for (int jb = 0; jb < nblk; ++jb) {
+        const int key0 = jb * BLK;
+        // S^T = K_j Q^T, 16 keys per tile, two tiles per slot
+        f32x4 sacc[kKT];
+#pragma unroll
+        for (int s = 0; s < kSPB; ++s) {
+            wait_slot(consumed);
+            const char* slot = ring + (consumed % C::kRing) * C::kSlotBytes;
+#pragma unroll
+            for (int t2 = 0; t2 < 2; ++t2) {
+                f32x4 acc = {};
+#pragma unroll
+                for (int kk = 0; kk < kDK; ++kk) {
+                    const u32x4 a = *reinterpret_cast<const u32x4*>(
+                        slot + krow + t2 * 16 * C::kRowBytes + 16 * ((4 * kk + grp) ^ kx));
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a), as_bf16x8(qop[kk]), acc, 0, 0, 0);
+                }
+                sacc[2 * s + t2] = acc;
+            }
+            next_slot();
+        }
+        // mask keys past kmax; register i of tile kt holds key key0 + 16*kt + 4*grp + i
+        if (key0 + BLK - 1 > kmax_lo) {
+            asm volatile("" ::: "memory");
+            const int lim = kmax - key0 - 4 * grp;
+#pragma unroll
+            for (int kt = 0; kt < kKT; ++kt)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (16 * kt + i > lim) sacc[kt][i] = ninf;
+        }
+        float amax = ninf;
+#pragma unroll
+        for (int kt = 0; kt < kKT; ++kt)
+            amax = __builtin_fmaxf(amax, __builtin_fmaxf(__builtin_fmaxf(sacc[kt][0], sacc[kt][1]),
+                                                         __builtin_fmaxf(sacc[kt][2], sacc[kt][3])));
+        amax = __builtin_fmaxf(amax, __shfl_xor(amax, 16, 64));
+        amax = __builtin_fmaxf(amax, __shfl_xor(amax, 32, 64));
+
+        // block-aware precision rescaling (Alg. 1), per row (see the prefill kernel)
+        const bool vis = amax != ninf;
+        const bool forced = (jb < p.n_b0) || (m == ninf);
+        const float tq = hif8::round(__builtin_fmaf(amax, c, -m));
+        const bool restart = forced || (ceilf(tq) > lam);
+        const float m_hi = __builtin_fmaxf(m, ceilf(amax * c));
+        const float m_new = vis ? (restart ? m_hi : m + __builtin_fmaxf(0.0f, ceilf(tq))) : m;
+        const float ref_new = vis ? (restart ? m_hi : m) : ref;
+        const bool b1 = vis && (jb >= p.n_b0);
+        n_visit += b1 ? 1u : 0u;
+        n_restart += (b1 && restart) ? 1u : 0u;
+        const float fac = (ref == ninf) ? 1.0f : exp2_int(ref - ref_new);
+        if (__any(fac != 1.0f)) {
+#pragma unroll
+            for (int t = 0; t < kDT; ++t)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) oacc[t][i] *= fac;
+        }
+        dl *= fac;
+        m = m_new;
+        ref = ref_new;
+        const float nref = (ref == ninf) ? 0.0f : -ref;
+
+        // P = HiF8(2^HiF8(T)); a 32-key chunk (tiles 2s, 2s+1) forms one B
+        // operand: slots 0..3 = keys 4*grp + i, slots 4..7 = keys 16 + 4*grp + i
+        const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+        for (int s = 0; s < kSPB; ++s) {
+            u32x4 pop;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int kt = 2 * s + (e >> 1);
+                const float t0 = __builtin_fmaf(sacc[kt][2 * (e & 1)], c, nref);
+                const float t1 = __builtin_fmaf(sacc[kt][2 * (e & 1) + 1], c, nref);
+                const uint32_t p0 = tab[hif8::f2u(t0) >> kTabShift];
+                const uint32_t p1 = tab[hif8::f2u(t1) >> kTabShift];
+                const uint32_t w = p0 | (p1 << 16);
+                pop[e] = w;
+                dl = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), ones, dl, false);
+            }
+            // X^T += V^T P^T for this slot's 32 keys
+            wait_slot(consumed);
+            const char* slot = ring + (consumed % C::kRing) * C::kSlotBytes;
+#pragma unroll
+            for (int t = 0; t < kDT; ++t) {
+                const char* pa = slot + vrow + 16 * (((16 * t + vd0) >> 3) ^ vx);
+                const s16x4 va = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LDS_PTR(s16x4, pa));
+                const s16x4 vb = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LDS_PTR(s16x4, pa + 16 * C::kRowBytes));
+                const u32x4 a = {__builtin_bit_cast(u32x2, va)[0], __builtin_bit_cast(u32x2, va)[1],
+                                 __builtin_bit_cast(u32x2, vb)[0], __builtin_bit_cast(u32x2, vb)[1]};
+                oacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a), as_bf16x8(pop), oacc[t], 0, 0, 0);
+            }
+            next_slot();
+        }
+    }
+
+    // epilogue: O = X / dX, lse = ln2 (ref + log2 dX); the 4 lanes of a
+    // query hold disjoint d rows 16*t + 4*grp + i
+    float d = dl + __shfl_xor(dl, 16, 64);
+    d += __shfl_xor(d, 32, 64);
+    if (!row_ok) return;
+    float* orow = p.o + (((long long)b * p.Hq + h) * p.Sq + r) * D;
+    const bool empty = (ref == ninf);
+    const float inv = empty ? 0.0f : 1.0f / d;
+#pragma unroll
+    for (int t = 0; t < kDT; ++t) {
+        f32x4 v;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = oacc[t][e] * inv;
+        *reinterpret_cast<f32x4*>(orow + 16 * t + 4 * grp) = v;
+    }
+    if (grp == 0) {
+        if (p.lse) p.lse[((long long)b * p.Hq + h) * p.Sq + r] = empty ? ninf : 0.69314718055994531f * (ref + log2f(d));
+        if (p.counters && n_visit) {
+            atomicAdd(p.counters + 2 * ((long long)b * p.Hq + h) + 0, (unsigned long long)n_restart);
+            atomicAdd(p.counters + 2 * ((long long)b * p.Hq + h) + 1, (unsigned long long)n_visit);
+        }
+    }
+}
+
+template <int D, int BLK>
+hipError_t launch_dec(const AttnParams& p, hipStream_t st)
+{
+    using C = DCfg<D>;
+    static bool attr_set = false;
+    if (!attr_set) {
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&baps_attn_decode_kernel<D, BLK>),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, C::kLdsBytes);
+        if (e != hipSuccess) return e;
+        attr_set = true;
+    }
+    const long long flat = (long long)p.Sq * (p.Hq / p.Hkv);
+    const dim3 grid((unsigned)((flat + kRows - 1) / kRows), (unsigned)p.Hkv, (unsigned)p.B);
+    hipLaunchKernelGGL((baps_attn_decode_kernel<D, BLK>), grid, dim3(64), C::kLdsBytes, st, p);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_attention_decode(const AttnParams& p, int D, int block, hipStream_t st)
+{
+    if (D == 64 && block == 32) return launch_dec<64, 32>(p, st);
+    if (D == 64 && block == 64) return launch_dec<64, 64>(p, st);
+    if (D == 64 && block == 128) return launch_dec<64, 128>(p, st);
+    if (D == 128 && block == 32) return launch_dec<128, 32>(p, st);
+    if (D == 128 && block == 64) return launch_dec<128, 64>(p, st);
+    if (D == 128 && block == 128) return launch_dec<128, 128>(p, st);
+    return hipErrorInvalidValue;
+}
+
+}  // namespace baps

@@ -358,9 +358,9 @@ hipError_t launch_one(const AttnParams& p, hipStream_t st)
 template <int D, int BLK>
 hipError_t launch_d_blk(const AttnParams& p, hipStream_t st)
 {
-    // few rows per key/value head (decode, short queries): one wave per workgroup
+    // few rows per key/value head (decode, short queries): the HBM-streaming kernel
     const long long flat = (long long)p.Sq * (p.Hq / p.Hkv);
-    if (flat <= 64) return launch_one<D, BLK, 1>(p, st);
+    if (flat <= 64) return launch_attention_decode(p, D, BLK, st);
     return launch_one<D, BLK, 8>(p, st);
 }
 

@@ -71,5 +71,6 @@ hipError_t launch_hif8_encode(const float* x, uint8_t* codes, long long n, bool 
 hipError_t launch_hif8_decode(const uint8_t* codes, float* x, long long n, hipStream_t st);
 hipError_t launch_softmax_block(const SoftmaxBlockParams& p, hipStream_t st);
 hipError_t launch_attention(const AttnParams& p, int D, int block, hipStream_t st);
+hipError_t launch_attention_decode(const AttnParams& p, int D, int block, hipStream_t st);
 
 }  // namespace baps
