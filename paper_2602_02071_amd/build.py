@@ -20,7 +20,8 @@ HIPCC_FLAGS = [
 ]
 # per-source extra flags.  The fused attention kernel takes finite scores (or
 # -inf for masked keys) only, so its max reductions need no NaN quieting.
-EXTRA_FLAGS = {"attn_fwd.hip": ["-fno-honor-nans"], "attn_decode.hip": ["-fno-honor-nans"]}
+EXTRA_FLAGS = {"attn_fwd.hip": ["-fno-honor-nans"], "attn_decode.hip": ["-fno-honor-nans"],
+               "softmax_block.hip": ["-fno-honor-nans"]}
 
 
 def sources():

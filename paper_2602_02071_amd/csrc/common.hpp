@@ -59,6 +59,32 @@ __device__ __forceinline__ float wave_max(float v)
     return v;
 }
 
+// Wave-uniform maximum with DPP row ops (quad permutes and mirrors inside
+// each row of 16 lanes, then row broadcasts): no LDS round trips.
+__device__ __forceinline__ float dpp_max_step(float v, int ctrl, int row_mask)
+{
+    const int o = __builtin_bit_cast(int, v);
+    switch (ctrl) {   // the DPP control must be a compile-time constant
+    case 0xB1: return fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(o, o, 0xB1, 0xF, 0xF, false)));
+    case 0x4E: return fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(o, o, 0x4E, 0xF, 0xF, false)));
+    case 0x141: return fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(o, o, 0x141, 0xF, 0xF, false)));
+    case 0x140: return fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(o, o, 0x140, 0xF, 0xF, false)));
+    case 0x142: return fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(o, o, 0x142, 0xA, 0xF, false)));
+    default: return fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(o, o, 0x143, 0xC, 0xF, false)));
+    }
+}
+
+__device__ __forceinline__ float wave_max_uniform(float v)
+{
+    v = dpp_max_step(v, 0xB1, 0xF);     // lane ^ 1
+    v = dpp_max_step(v, 0x4E, 0xF);     // lane ^ 2
+    v = dpp_max_step(v, 0x141, 0xF);    // mirror within 8
+    v = dpp_max_step(v, 0x140, 0xF);    // mirror within 16
+    v = dpp_max_step(v, 0x142, 0xA);    // row 0 -> 1, row 2 -> 3
+    v = dpp_max_step(v, 0x143, 0xC);    // row 1 -> 2 and 3
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
+}
+
 __device__ __forceinline__ float wave_sum(float v)
 {
 #pragma unroll

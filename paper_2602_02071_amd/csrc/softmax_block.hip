@@ -62,7 +62,7 @@ __global__ __launch_bounds__(kThreads) void softmax_block_kernel(SoftmaxBlockPar
             float M = ninf;
 #pragma unroll
             for (int t = 0; t < kBPL; ++t) M = fmaxf(M, cur[b * kBPL + t]);
-            M = wave_max(M);
+            M = wave_max_uniform(M);
 
             // Alg. 1: B0 blocks always take the high-precision path; B1 blocks
             // test ceil(rowmax T) > lambda with T = S - m~ cast to 8 bits.
@@ -130,10 +130,161 @@ __global__ __launch_bounds__(kThreads) void softmax_block_kernel(SoftmaxBlockPar
     }
 }
 
+// Row-group variant for 16-byte aligned rows whose length is a multiple of 4
+// and blocks of at most 256 columns: a wave owns 4 rows and each row is a
+// DPP row of 16 lanes, so the per-block maximum is 4 in-row DPP steps and the
+// per-block state update runs for 4 rows at once.  A lane holds 4 adjacent
+// columns per 64-column group: fp32x4 loads and 4-code stores, contiguous
+// per row.
+__device__ __forceinline__ float row16_max(float v)
+{
+    int o = __builtin_bit_cast(int, v);
+    v = fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(o, o, 0xB1, 0xF, 0xF, false)));
+    o = __builtin_bit_cast(int, v);
+    v = fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(o, o, 0x4E, 0xF, 0xF, false)));
+    o = __builtin_bit_cast(int, v);
+    v = fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(o, o, 0x141, 0xF, 0xF, false)));
+    o = __builtin_bit_cast(int, v);
+    return fmaxf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(o, o, 0x140, 0xF, 0xF, false)));
+}
+
+__device__ __forceinline__ float row16_sum(float v)
+{
+    int o = __builtin_bit_cast(int, v);
+    v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(o, o, 0xB1, 0xF, 0xF, false));
+    o = __builtin_bit_cast(int, v);
+    v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(o, o, 0x4E, 0xF, 0xF, false));
+    o = __builtin_bit_cast(int, v);
+    v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(o, o, 0x141, 0xF, 0xF, false));
+    o = __builtin_bit_cast(int, v);
+    return v + __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(o, o, 0x140, 0xF, 0xF, false));
+}
+
+constexpr int kRowsPerWave4 = 4;
+constexpr int kRows4PerBlock = kRowsPerWave4 * (kThreads / 64);
+
+template <int BLOCK>
+__global__ __launch_bounds__(kThreads) void softmax_block4_kernel(SoftmaxBlockParams p)
+{
+    __shared__ uint32_t tab[kTabEntries];
+    for (int i = threadIdx.x; i < kTabEntries; i += kThreads) tab[i] = p.tab[i];
+    __syncthreads();
+
+    constexpr int kCh = BLOCK < 256 ? 256 : BLOCK;        // columns per row per step
+    constexpr int kG = kCh / 64;                          // fp32x4 groups per lane per step
+    constexpr int kGPB = BLOCK / 64;                      // groups per block (>= 1)
+    constexpr int kBPS = kCh / BLOCK;                     // blocks per step
+    const int lane = threadIdx.x & 63;
+    const int sub = lane & 15;
+    const long long row = (long long)blockIdx.x * kRows4PerBlock + (threadIdx.x >> 6) * kRowsPerWave4 + (lane >> 4);
+    const bool row_ok = row < p.rows;                     // whole DPP rows agree
+    const long long rr = row_ok ? row : 0;
+
+    const long long cols = p.cols;
+    const long long nblk = (cols + BLOCK - 1) / BLOCK;
+    const float* S = p.s + rr * p.ld;
+    uint8_t* code = p.codes + rr * cols;
+    int32_t* refs_out = p.ref_shift + rr * nblk;
+    const float ninf = -__builtin_huge_valf();
+
+    float m = ninf, dl = 0.0f, myref = ninf;
+    long long j = 0;
+    f32x4 cur[kG], nxt[kG];
+    auto load = [&](f32x4* v, long long c0) {
+#pragma unroll
+        for (int i = 0; i < kG; ++i) {
+            const long long c = c0 + 64 * i + 4 * sub;
+            v[i] = (row_ok && c < cols) ? __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(S + c))
+                                        : f32x4{ninf, ninf, ninf, ninf};
+        }
+    };
+    load(cur, 0);
+    for (long long c0 = 0; c0 < cols; c0 += kCh) {
+        if (c0 + kCh < cols) load(nxt, c0 + kCh);
+#pragma unroll
+        for (int bb = 0; bb < kBPS; ++bb) {
+            if (j >= nblk) break;
+            float M = ninf;
+#pragma unroll
+            for (int gi = 0; gi < kGPB; ++gi)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) M = fmaxf(M, cur[bb * kGPB + gi][e]);
+            M = row16_max(M);
+            bool restart;
+            float tq = ninf;
+            if (j < p.n_b0) {
+                restart = true;
+            } else {
+                if (M != ninf) tq = hif8::round(M - m);
+                restart = ceilf(tq) > (float)p.lambda;
+            }
+            const float m_new = restart ? fmaxf(m, ceilf(M)) : m + fmaxf(0.0f, ceilf(tq));
+            const float ref = restart ? m_new : m;
+            const float alpha = (m == ninf) ? 0.0f : exp2_int(m - m_new);
+            const float beta = (ref == ninf) ? 0.0f : exp2_int(ref - m_new);
+            float rowsum = 0.0f;
+#pragma unroll
+            for (int gi = 0; gi < kGPB; ++gi) {
+                uint32_t word = 0;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float sv = cur[bb * kGPB + gi][e];
+                    const float T = (sv == ninf || ref == ninf) ? ninf : sv - ref;
+                    const uint32_t ent = tab[hif8::f2u(T) >> kTabShift];
+                    word |= (ent & 0xffu) << (8 * e);
+                    rowsum += hif8::u2f(ent & 0xffffff00u);
+                }
+                const long long c = c0 + (long long)bb * BLOCK + 64 * gi + 4 * sub;
+                if (row_ok && c < cols) *reinterpret_cast<uint32_t*>(code + c) = word;
+            }
+            dl = alpha * dl + beta * rowsum;
+            m = m_new;
+            if (row_ok && p.restarted && sub == 0) p.restarted[rr * nblk + j] = restart ? 1 : 0;
+            if (sub == (int)(j & 15)) myref = ref;
+            if ((j & 15) == 15 || j == nblk - 1) {
+                if (nblk > 16 && row_ok) {      // park the group's references until m is final
+                    const long long idx = (j & ~15LL) + sub;
+                    if (idx < nblk) refs_out[idx] = (int32_t)hif8::f2u(myref);
+                }
+            }
+            ++j;
+        }
+#pragma unroll
+        for (int i = 0; i < kG; ++i) cur[i] = nxt[i];
+    }
+    const float d = row16_sum(dl);
+    if (!row_ok) return;
+    if (sub == 0) {
+        p.m_final[rr] = m;
+        p.d_final[rr] = d;
+    }
+    auto shift = [&](float ref) -> int32_t {
+        if (ref == ninf || m == ninf) return INT32_MIN;
+        return (int32_t)fmaxf(ref - m, -2147483520.0f);
+    };
+    if (nblk <= 16) {
+        if (sub < nblk) refs_out[sub] = shift(myref);
+    } else {
+        for (long long idx = sub; idx < nblk; idx += 16)
+            refs_out[idx] = shift(hif8::u2f((uint32_t)refs_out[idx]));
+    }
+}
+
 }  // namespace
 
 hipError_t launch_softmax_block(const SoftmaxBlockParams& p, hipStream_t st)
 {
+    const bool vec = ((uintptr_t)p.s % 16 == 0) && (p.ld % 4 == 0) && (p.cols % 4 == 0) &&
+                     ((uintptr_t)p.codes % 4 == 0) && p.block <= 256;
+    if (vec) {
+        const dim3 grid4((unsigned)((p.rows + kRows4PerBlock - 1) / kRows4PerBlock));
+        switch (p.block) {
+        case 64: hipLaunchKernelGGL(softmax_block4_kernel<64>, grid4, dim3(kThreads), 0, st, p); break;
+        case 128: hipLaunchKernelGGL(softmax_block4_kernel<128>, grid4, dim3(kThreads), 0, st, p); break;
+        default: hipLaunchKernelGGL(softmax_block4_kernel<256>, grid4, dim3(kThreads), 0, st, p); break;
+        }
+        return hipGetLastError();
+    }
     const dim3 grid((unsigned)((p.rows + kRowsPerBlock - 1) / kRowsPerBlock));
     switch (p.block) {
     case 64: hipLaunchKernelGGL(softmax_block_kernel<64>, grid, dim3(kThreads), 0, st, p); break;

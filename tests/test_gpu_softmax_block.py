@@ -90,3 +90,13 @@ def test_golden_walkthrough_on_gpu():
         assert refs[0].tolist() == c["ref_shift"]
         assert rs[0].tolist() == c["restarted"]
         assert m[0] == c["m_final"] and d[0] == c["d_final"]
+
+
+@pytest.mark.parametrize("block,cols", [(64, 2560), (128, 2560), (256, 4096 + 256), (128, 132)])
+def test_row_group_path_many_blocks(block, cols):
+    # 16-byte aligned rows with a multiple-of-4 length take the 4-rows-per-wave
+    # kernel; > 16 blocks per row exercises its reference parking
+    s = random_scores(37, cols, seed=cols + block, std=6.0, masked_frac=0.02)
+    s[5, :] = -np.inf
+    s[6, : block] = -np.inf
+    _compare(s, block)
