@@ -23,7 +23,8 @@ sys.path.insert(0, ROOT)
 METRIC = "BAPS attention fwd TFLOP/s + % bf16 MFMA peak (prefill); decode HBM GB/s"
 PEAK_BF16_TFLOPS = 2500.0        # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0            # MI355X HBM3E
-KERNEL_SRC = os.path.join(ROOT, "paper_2602_02071_amd", "csrc", "attn_fwd.hip")
+CSRC = os.path.join(ROOT, "paper_2602_02071_amd", "csrc")
+KERNEL_SRC = {"attn_fwd_prefill": "attn_fwd.hip", "attn_fwd_decode": "attn_decode.hip"}
 
 
 def _src_hash(path):
@@ -31,8 +32,10 @@ def _src_hash(path):
 
 
 def _traffic(kernel_tag):
-    """HBM bytes per launch from the committed rocprofv3 counter summary,
-    if it was taken on the current kernel source (else None)."""
+    """HBM bytes per launch from the committed rocprofv3 counter summary
+    (FETCH_SIZE + WRITE_SIZE, scaled by the same counters' reading for a
+    plain copy of known size), if it was taken on the current kernel source;
+    else None."""
     path = os.path.join(ROOT, "profiles", f"{kernel_tag}_traffic.json")
     if not os.path.exists(path):
         return None
@@ -40,7 +43,7 @@ def _traffic(kernel_tag):
         rec = json.load(open(path))
     except ValueError:
         return None
-    if rec.get("source_sha256_16") != _src_hash(KERNEL_SRC):
+    if rec.get("source_sha256_16") != _src_hash(os.path.join(CSRC, KERNEL_SRC[kernel_tag])):
         return None
     return rec.get("hbm_bytes_per_launch")
 
@@ -83,15 +86,57 @@ def run_attention(cfg, steps, warmup):
     return w, (q, k, v), wall, per
 
 
+def boundary_kernels(steps=10):
+    """Throughput of the standalone boundary kernels on HBM-sized inputs:
+    hif8_encode / hif8_decode over 2^28 elements (1 GiB of fp32, beyond the
+    256 MiB Infinity Cache) and baps_softmax_block over 16384 x 8192 scores
+    with 128-column blocks.  Bytes are algorithmic (each input read once,
+    each output written once)."""
+    import torch
+    import paper_2602_02071_amd as baps
+
+    def timed(fn):
+        _, per = _time_launches(fn, steps, 2)
+        return float(np.median(per)) * 1e-3
+
+    res = {}
+    n = 1 << 28
+    g = torch.Generator(device="cuda:0").manual_seed(7)
+    x = torch.randn(n, device="cuda:0", generator=g) * 10
+    codes = torch.empty(n, dtype=torch.uint8, device="cuda:0")
+    t = timed(lambda: baps.hif8_encode(x, codes, n))
+    res["hif8_encode"] = {"elements": n, "us": t * 1e6, "GB/s": 5 * n / t / 1e9, "frac_of_hbm_peak": 5 * n / t / 1e9 / PEAK_HBM_GBS}
+    t = timed(lambda: baps.hif8_decode(codes, x, n))
+    res["hif8_decode"] = {"elements": n, "us": t * 1e6, "GB/s": 5 * n / t / 1e9, "frac_of_hbm_peak": 5 * n / t / 1e9 / PEAK_HBM_GBS}
+    del x, codes
+    rows, cols, blk = 16384, 8192, 128
+    nb = cols // blk
+    s = torch.randn(rows, cols, device="cuda:0", generator=g) * 4
+    pc = torch.empty(rows, cols, dtype=torch.uint8, device="cuda:0")
+    rs = torch.empty(rows, nb, dtype=torch.int32, device="cuda:0")
+    mf = torch.empty(rows, device="cuda:0")
+    df = torch.empty(rows, device="cuda:0")
+    rst = torch.empty(rows, nb, dtype=torch.uint8, device="cuda:0")
+    t = timed(lambda: baps.baps_softmax_block(s, rows, cols, cols, blk, 1, 1, 0, pc, rs, mf, df, rst))
+    byt = rows * cols * 5 + rows * nb * 5 + rows * 8
+    res["baps_softmax_block"] = {"rows": rows, "cols": cols, "block": blk, "us": t * 1e6, "GB/s": byt / t / 1e9,
+                                 "frac_of_hbm_peak": byt / t / 1e9 / PEAK_HBM_GBS}
+    return res
+
+
 def cpu_baseline(w, qkv, seconds_hint=True):
     """The oracle, as it stands, on a bounded sample of the same workload."""
     import oracle
     from paper_2602_02071_amd.workloads import sample_rows
     q, k, v = qkv
-    heads = range(0, w.Hq, 2) if w.Sq > 1 else range(w.Hq)
-    rows = sample_rows(w, every=1, tile=1, heads=heads) if w.Sq > 1 else None
-    if w.Sq == 1:
+    if w.Sq > 1:
+        # whole workload if it is small enough, else every other head
+        heads = range(w.Hq) if w.flops <= 2e11 else range(0, w.Hq, 2)
+        rows = sample_rows(w, every=1, tile=1, heads=heads)
+        what = "all rows" if len(heads) == w.Hq else "every other head, all rows"
+    else:
         rows = np.arange(0, w.B * w.Hq, 8, dtype=np.int64)
+        what = "every 8th decode row"
     nthreads = oracle.default_threads()
     t0 = time.perf_counter()
     oracle.attention(q, k, v, w.B, w.Hq, w.Hkv, w.Sq, w.Sk, w.D, w.causal, w.block, rows=rows,
@@ -100,8 +145,7 @@ def cpu_baseline(w, qkv, seconds_hint=True):
     r = rows % w.Sq
     vis = np.minimum(w.Sk, r + w.Sk - w.Sq + 1) if w.causal else np.full(r.shape, w.Sk)
     flops = 4.0 * w.D * float(np.clip(vis, 0, w.Sk).sum())
-    sample = (f"{len(rows)} of {w.B * w.Hq * w.Sq} query rows ({'every other head, all rows' if w.Sq > 1 else 'every 8th row'})"
-              f", {dt:.1f} s")
+    sample = f"{len(rows)} of {w.B * w.Hq * w.Sq} query rows ({what}), {dt:.1f} s"
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": nthreads, "kind": "oracle", "sample": sample}
 
 
@@ -113,6 +157,7 @@ def main():
     ap.add_argument("--config", type=int, default=2, help="workload 1..5 (2 = Llama-3-8B prefill)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--no-boundary", action="store_true", help="skip the codec / softmax-block kernels")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -153,8 +198,11 @@ def main():
         ms_d = float(np.mean(per_d))
         gbs = wd.bytes_qkvo / (ms_d * 1e-3) / 1e9
         out["decode"] = {"workload": wd.name, "ms_per_step": ms_d, "value": gbs, "unit": "GB/s",
-                         "frac_of_hbm_peak": gbs / PEAK_HBM_GBS, "tokens_per_s": wd.B / (ms_d * 1e-3),
-                         "traffic": _traffic("attn_fwd_decode")}
+                         "tokens_per_s": wd.B / (ms_d * 1e-3),
+                         "roofline": {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                                      "frac": gbs / PEAK_HBM_GBS, "traffic": _traffic("attn_fwd_decode")}}
+    if not args.no_boundary:
+        out["boundary"] = boundary_kernels()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, qkv)
     if args.calib_copy_mib:

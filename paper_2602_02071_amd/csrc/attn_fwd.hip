@@ -117,9 +117,30 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
     const int G = p.Hq / p.Hkv;
     const int flat_rows = p.Sq * G;
     const int ntiles = (flat_rows + C::kTileRows - 1) / C::kTileRows;
-    const int tile = ntiles - 1 - (int)blockIdx.x;          // longest causal tiles first
-    const int g = blockIdx.y;
-    const int b = blockIdx.z;
+    // Work item (tile, key/value head, batch).  Workgroups are dealt to the 8
+    // XCDs round-robin by linear id, each XCD with its own L2; when the
+    // (batch, kv head) count is a multiple of 8, the linear id L is mapped so
+    // that every tile of a kv head runs on the same XCD (L % 8 picks the head
+    // class) and its K/V is fetched into one L2 only.  Within an XCD the
+    // longest causal tiles go first.
+    int tile, g, b;
+    {
+        const int L = (int)(blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z));
+        const int heads = p.B * p.Hkv;
+        int t_rev, hk;
+        if (heads % 8 == 0) {
+            const int hpx = heads / 8;                      // heads per XCD
+            const int k = L >> 3;
+            hk = (L & 7) + 8 * (k % hpx);
+            t_rev = k / hpx;
+        } else {
+            t_rev = L % ntiles;
+            hk = L / ntiles;
+        }
+        tile = ntiles - 1 - t_rev;
+        g = hk % p.Hkv;
+        b = hk / p.Hkv;
+    }
     const uint16_t* kbase = p.k + ((long long)b * p.Hkv + g) * (long long)p.Sk * D;
     const uint16_t* vbase = p.v + ((long long)b * p.Hkv + g) * (long long)p.Sk * D;
 
