@@ -64,6 +64,36 @@ struct Cfg {
     static constexpr int kLdsBytes = 4 * kTileBytes;
 };
 
+// maximum of n values as a tree of 3-input maxima (short dependency chain)
+template <int N>
+__device__ __forceinline__ float tree_max(float* v)
+{
+    int n = N;
+#pragma unroll
+    for (int lvl = 0; lvl < 6; ++lvl) {
+        if (n == 1) break;
+        const int m = (n + 2) / 3;
+#pragma unroll
+        for (int i = 0; i < m; ++i) {
+            const int a = 3 * i, b = 3 * i + 1, c = 3 * i + 2;
+            v[i] = c < n ? __builtin_fmaxf(__builtin_fmaxf(v[a], v[b]), v[c]) : (b < n ? __builtin_fmaxf(v[a], v[b]) : v[a]);
+        }
+        n = m;
+    }
+    return v[0];
+}
+
+// value of lane l^32 (v_permlane32_swap: no LDS round trip)
+__device__ __forceinline__ float swap_halves(float x)
+{
+    const uint32_t u = __builtin_bit_cast(uint32_t, x);
+    const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+    // element 0: lanes 0..31 keep their value, lanes 32..63 receive lanes 0..31;
+    // element 1: lanes 0..31 receive lanes 32..63, lanes 32..63 keep theirs
+    const uint32_t r0 = r[0], r1 = r[1];
+    return __builtin_bit_cast(float, (threadIdx.x & 32) ? r0 : r1);
+}
+
 // One wave-wide asynchronous global->LDS load: lane l's 16 bytes at gptr land
 // at LDS byte lds_base + 16*l.  Issued as inline assembly so that the compiler
 // does not guard every later LDS read with a wait on these loads; the kernel
@@ -262,13 +292,18 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
                 for (int i = 0; i < 16; ++i)
                     if (kt * 32 + 8 * (i / 4) + (i % 4) > lim) sacc[kt][i] = ninf;
         }
-        // row maximum of the raw dot products (the scale c > 0 is monotone)
-        float amax = ninf;
+        // row maximum of the raw dot products (the scale c > 0 is monotone):
+        // a 3-way tree over this lane's 16*kKT scores, then lanes l and l^32
+        float amax;
+        {
+            float mx[16 * kKT];
 #pragma unroll
-        for (int kt = 0; kt < kKT; ++kt)
+            for (int kt = 0; kt < kKT; ++kt)
 #pragma unroll
-            for (int i = 0; i < 16; i += 2) amax = __builtin_fmaxf(amax, __builtin_fmaxf(sacc[kt][i], sacc[kt][i + 1]));
-        amax = __builtin_fmaxf(amax, __shfl_xor(amax, 32, 64));
+                for (int i = 0; i < 16; ++i) mx[16 * kt + i] = sacc[kt][i];
+            amax = tree_max<16 * kKT>(mx);
+            amax = __builtin_fmaxf(amax, swap_halves(amax));
+        }
 
         // block-aware precision rescaling (Alg. 1), per row, branch-free.
         // B0 blocks (and a first block with m = -inf) take the high-precision
