@@ -16,6 +16,8 @@ using namespace baps;
 // input and rounded back to 8 bits), as fp32 bits with the HiF8 code of P
 // in the low byte.  Lives in static device memory, one copy per device.
 __device__ uint32_t g_score_table[kTabEntries];
+// The compact code table of the fused attention kernels (see common.hpp).
+__device__ uint8_t g_code_table[kCodeEntries];
 
 // HiF8 value of a double, rounded once: truncating to fp32 toward zero keeps
 // the sign, the exponent and the leading mantissa bits that decide a
@@ -40,8 +42,23 @@ float hif8_exp2(float t)
     return hif8_round_double(y);
 }
 
+// byte c = ((e + 23) << 3) | m of a HiF8 value p = 2^e (1 + m/8) >= 0 (0 for
+// p = 0); values beyond 2^kCodeMaxLambda (unreachable for lambda <=
+// kCodeMaxLambda) saturate to 255
+uint8_t linear_code(float p)
+{
+    if (p == 0.0f) return 0;
+    int e = 0;
+    const float fr = std::frexp(p, &e);              // p = fr * 2^e, fr in [0.5, 1)
+    e -= 1;
+    const int m = (int)std::lround((2.0f * fr - 1.0f) * 8.0f);
+    if (e > kCodeMaxLambda) return 255;
+    return (uint8_t)(((e + 23) << 3) | m);
+}
+
 struct Table {
     uint32_t e[kTabEntries];
+    uint8_t code[kCodeEntries];
     Table()
     {
         for (uint32_t i = 0; i < (uint32_t)kTabEntries; ++i) {
@@ -50,6 +67,7 @@ struct Table {
             const uint32_t pb = hif8::f2u(p);
             e[i] = (pb & 0xffffff00u) | hif8::encode(p, true);
         }
+        for (int i = 0; i < kCodeEntries; ++i) code[i] = linear_code(hif8::u2f(e[kCodeLo + i] & 0xffffff00u));
     }
 };
 
@@ -62,8 +80,9 @@ const Table& host_table()
 constexpr int kMaxDevices = 64;
 std::mutex g_mutex;
 const uint32_t* g_dev_table[kMaxDevices] = {};
+const uint8_t* g_dev_code[kMaxDevices] = {};
 
-int table_on_current_device(const uint32_t** out)
+int table_on_current_device(const uint32_t** out, const uint8_t** code = nullptr)
 {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return BAPS_HIP_ERROR;
@@ -75,9 +94,15 @@ int table_on_current_device(const uint32_t** out)
             return BAPS_HIP_ERROR;
         void* ptr = nullptr;
         if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(g_score_table)) != hipSuccess || !ptr) return BAPS_HIP_ERROR;
+        if (hipMemcpyToSymbol(HIP_SYMBOL(g_code_table), t.code, sizeof(t.code), 0, hipMemcpyHostToDevice) != hipSuccess)
+            return BAPS_HIP_ERROR;
+        void* cptr = nullptr;
+        if (hipGetSymbolAddress(&cptr, HIP_SYMBOL(g_code_table)) != hipSuccess || !cptr) return BAPS_HIP_ERROR;
+        g_dev_code[dev] = static_cast<const uint8_t*>(cptr);
         g_dev_table[dev] = static_cast<const uint32_t*>(ptr);
     }
     *out = g_dev_table[dev];
+    if (code) *code = g_dev_code[dev];
     return BAPS_OK;
 }
 
@@ -99,9 +124,11 @@ int attention_impl(const void* q, const void* k, const void* v, float* o, float*
     if (!(D == 64 || D == 128) || !(block == 32 || block == 64 || block == 128)) return BAPS_UNSUPPORTED;
     if ((long long)Sq * (Hq / Hkv) > 0x7fffffffLL || Hkv > 65535 || B > 65535) return BAPS_UNSUPPORTED;
     const uint32_t* tab = nullptr;
-    int st = table_on_current_device(&tab);
+    const uint8_t* ctab = nullptr;
+    int st = table_on_current_device(&tab, &ctab);
     if (st) return st;
     AttnParams p;
+    p.ctab = ctab;
     p.q = static_cast<const uint16_t*>(q);
     p.k = static_cast<const uint16_t*>(k);
     p.v = static_cast<const uint16_t*>(v);

@@ -124,13 +124,16 @@ __device__ __forceinline__ void load_tile(const uint16_t* base, int key0, int Sk
     }
 }
 
-template <int D, int BLK, int NW>
+template <int D, int BLK, int NW, bool CT>
 __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
 {
     static_assert(D == 64 || D == 128, "head dimension");
     static_assert(BLK % 32 == 0 && BLK <= 128, "key block");
     using C = Cfg<D, BLK, NW>;
-    __shared__ __attribute__((aligned(16))) uint16_t tab[kTabEntries];
+    // P lookup: the compact code table (lambda <= kCodeMaxLambda), else the
+    // bf16 half of the full score table
+    __shared__ __attribute__((aligned(16))) uint8_t ctab[CT ? kCodeHi + 1 : 1];
+    __shared__ __attribute__((aligned(16))) uint16_t tab[CT ? 1 : kTabEntries];
     extern __shared__ __attribute__((aligned(1024))) char tiles[];
     const uint32_t tiles_lds = (uint32_t)(uintptr_t)LDS_PTR(char, tiles);
 
@@ -184,7 +187,11 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
         load_tile<D, BLK, NW, false>(kbase, 0, p.Sk, tiles_lds, wave, lane);
         load_tile<D, BLK, NW, true>(vbase, 0, p.Sk, tiles_lds + C::kTileBytes, wave, lane);
     }
-    for (int i = tid; i < kTabEntries; i += C::kThreads) tab[i] = (uint16_t)(p.tab[i] >> 16);
+    if constexpr (CT) {
+        for (int i = tid; i < kCodeEntries; i += C::kThreads) ctab[kCodeLo + i] = p.ctab[i];
+    } else {
+        for (int i = tid; i < kTabEntries; i += C::kThreads) tab[i] = (uint16_t)(p.tab[i] >> 16);
+    }
 
     // this lane's query row: flat index f = r * G + h_local
     const int f = tile * C::kTileRows + wave * kRowsPerWave + j32;
@@ -346,9 +353,15 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
                 for (int e = 0; e < 4; ++e) {
                     const float t0 = __builtin_fmaf(sacc[kt][ch * 8 + 2 * e], c, nref);
                     const float t1 = __builtin_fmaf(sacc[kt][ch * 8 + 2 * e + 1], c, nref);
-                    const uint32_t p0 = tab[hif8::f2u(t0) >> kTabShift];
-                    const uint32_t p1 = tab[hif8::f2u(t1) >> kTabShift];
-                    const uint32_t w = p0 | (p1 << 16);
+                    uint32_t w;
+                    if constexpr (CT) {
+                        // two bf16 of P * 2^-kCodeBiasLog2
+                        const uint32_t i0 = min(max(hif8::f2u(t0) >> kTabShift, (uint32_t)kCodeLo), (uint32_t)kCodeHi);
+                        const uint32_t i1 = min(max(hif8::f2u(t1) >> kTabShift, (uint32_t)kCodeLo), (uint32_t)kCodeHi);
+                        w = ((uint32_t)ctab[i0] | ((uint32_t)ctab[i1] << 16)) << 4;
+                    } else {
+                        w = (uint32_t)tab[hif8::f2u(t0) >> kTabShift] | ((uint32_t)tab[hif8::f2u(t1) >> kTabShift] << 16);
+                    }
                     pop[ch][e] = w;
                     dl = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), ones, dl, false);
                 }
@@ -370,8 +383,10 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
         }
     }
 
-    // epilogue: O = X / dX, lse = ln2 (ref + log2 dX) = ln2 (m + log2 d)
+    // epilogue: O = X / dX, lse = ln2 (ref + log2 dX) = ln2 (m + log2 d);
+    // with the compact table X and dX carry the factor 2^-kCodeBiasLog2
     const float d = dl + __shfl_xor(dl, 32, 64);
+    const float dbias = CT ? (float)kCodeBiasLog2 : 0.0f;
     if (!row_ok) return;
     float* orow = p.o + (((long long)b * p.Hq + h) * p.Sq + r) * D;
     const bool empty = (ref == ninf);
@@ -386,7 +401,7 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
             *reinterpret_cast<f32x4*>(orow + t * 32 + q4 * 8 + half * 4) = v;
         }
     if (half == 0) {
-        if (p.lse) p.lse[((long long)b * p.Hq + h) * p.Sq + r] = empty ? ninf : 0.69314718055994531f * (ref + log2f(d));
+        if (p.lse) p.lse[((long long)b * p.Hq + h) * p.Sq + r] = empty ? ninf : 0.69314718055994531f * (ref + (log2f(d) + dbias));
         if (p.counters && n_visit) {
             atomicAdd(p.counters + 2 * ((long long)b * p.Hq + h) + 0, (unsigned long long)n_restart);
             atomicAdd(p.counters + 2 * ((long long)b * p.Hq + h) + 1, (unsigned long long)n_visit);
@@ -394,20 +409,20 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
     }
 }
 
-template <int D, int BLK, int NW>
+template <int D, int BLK, int NW, bool CT>
 hipError_t launch_one(const AttnParams& p, hipStream_t st)
 {
     using C = Cfg<D, BLK, NW>;
     static bool attr_set = false;
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&baps_attn_fwd_kernel<D, BLK, NW>),
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&baps_attn_fwd_kernel<D, BLK, NW, CT>),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, C::kLdsBytes);
         if (e != hipSuccess) return e;
         attr_set = true;
     }
     const long long flat = (long long)p.Sq * (p.Hq / p.Hkv);
     const dim3 grid((unsigned)((flat + C::kTileRows - 1) / C::kTileRows), (unsigned)p.Hkv, (unsigned)p.B);
-    hipLaunchKernelGGL((baps_attn_fwd_kernel<D, BLK, NW>), grid, dim3(C::kThreads), C::kLdsBytes, st, p);
+    hipLaunchKernelGGL((baps_attn_fwd_kernel<D, BLK, NW, CT>), grid, dim3(C::kThreads), C::kLdsBytes, st, p);
     return hipGetLastError();
 }
 
@@ -417,7 +432,8 @@ hipError_t launch_d_blk(const AttnParams& p, hipStream_t st)
     // few rows per key/value head (decode, short queries): the HBM-streaming kernel
     const long long flat = (long long)p.Sq * (p.Hq / p.Hkv);
     if (flat <= 64) return launch_attention_decode(p, D, BLK, st);
-    return launch_one<D, BLK, 8>(p, st);
+    if (p.lambda <= kCodeMaxLambda) return launch_one<D, BLK, 8, true>(p, st);
+    return launch_one<D, BLK, 8, false>(p, st);
 }
 
 }  // namespace

@@ -20,6 +20,23 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 constexpr int kTabEntries = 8192;
 constexpr int kTabShift = 19;
 
+// Compact code table of the fused attention kernels, for thresholds lambda
+// <= kCodeMaxLambda.  Indexed like the score table (bits 31..19 of T) but
+// clamped to [kCodeLo, kCodeHi]: every T <= lambda lands on an entry with the
+// same P, since P = 1 for |T| < 2^-5 (either sign; the clamp sends positive T
+// below 2^-5 to the entry of 2^-5) and P = 0 for T <= -32 (the clamp sends
+// -inf and every T <= -32 to the entry of -32).  An entry is the byte
+// c = ((e + 23) << 3) | m of P = 2^e (1 + m/8) (c = 0 for P = 0), chosen so
+// that c << 4 is the bf16 pattern of P * 2^-kCodeBiasLog2, exactly: e runs
+// over [-22, kCodeMaxLambda] and HiF8 keeps at most 3 mantissa bits.  In
+// practice the hit entries sit in a few dozen LDS dwords: the gathers are
+// free of bank conflicts.
+constexpr int kCodeLo = 0x7A0;           // T = +2^-5
+constexpr int kCodeHi = 0x1840;          // T = -32
+constexpr int kCodeEntries = kCodeHi - kCodeLo + 1;
+constexpr int kCodeBiasLog2 = 104;
+constexpr int kCodeMaxLambda = 8;
+
 struct AttnParams {
     const uint16_t* q;          // [B, Hq, Sq, D] bf16
     const uint16_t* k;          // [B, Hkv, Sk, D] bf16
@@ -27,6 +44,7 @@ struct AttnParams {
     float* o;                   // [B, Hq, Sq, D]
     float* lse;                 // [B, Hq, Sq] or null
     const uint32_t* tab;        // score table (device)
+    const uint8_t* ctab;        // compact code table (device), kCodeEntries bytes
     unsigned long long* counters;  // [B*Hq][2] restarted / visited B1 row-blocks, or null
     int B, Hq, Hkv, Sq, Sk;
     int causal, lambda, n_b0;
