@@ -48,8 +48,30 @@ def _traffic(kernel_tag):
     return rec.get("hbm_bytes_per_launch")
 
 
-def _time_launches(fn, steps, warmup):
+def _spin_up(fn, min_ms):
+    """Run fn back to back until at least min_ms of GPU time has passed, so
+    that the timed steps run at steady clocks (the GPU raises its clocks over
+    the first tens of milliseconds of sustained work).  Untimed."""
     import torch
+    if min_ms <= 0:
+        return 0.0
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    done = 0
+    while True:
+        for _ in range(10):
+            fn()
+        done += 10
+        e1.record()
+        torch.cuda.synchronize()
+        el = e0.elapsed_time(e1)
+        if el >= min_ms or done >= 20000:
+            return el
+
+
+def _time_launches(fn, steps, warmup, spinup_ms=0.0):
+    import torch
+    _spin_up(fn, spinup_ms)
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
@@ -67,7 +89,7 @@ def _time_launches(fn, steps, warmup):
     return wall, per
 
 
-def run_attention(cfg, steps, warmup):
+def run_attention(cfg, steps, warmup, spinup_ms=0.0):
     import torch
     import paper_2602_02071_amd as baps
     from paper_2602_02071_amd.workloads import make_workload
@@ -82,7 +104,7 @@ def run_attention(cfg, steps, warmup):
     def step():
         baps.baps_attention_fwd(qt, kt, vt, o, lse, w.B, w.Hq, w.Hkv, w.Sq, w.Sk, w.D, w.causal, w.block, stream)
 
-    wall, per = _time_launches(step, steps, warmup)
+    wall, per = _time_launches(step, steps, warmup, spinup_ms)
     return w, (q, k, v), wall, per
 
 
@@ -96,7 +118,7 @@ def boundary_kernels(steps=10):
     import paper_2602_02071_amd as baps
 
     def timed(fn):
-        _, per = _time_launches(fn, steps, 2)
+        _, per = _time_launches(fn, steps, 2, 50.0)
         return float(np.median(per)) * 1e-3
 
     res = {}
@@ -152,8 +174,10 @@ def cpu_baseline(w, qkv, seconds_hint=True):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--spinup-ms", type=float, default=200.0,
+                    help="untimed back-to-back launches before the warmup steps, to reach steady clocks")
     ap.add_argument("--config", type=int, default=2, help="workload 1..5 (2 = Llama-3-8B prefill)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
@@ -167,7 +191,7 @@ def main():
               file=sys.stderr)
         sys.exit(2)
 
-    w, qkv, wall, per = run_attention(args.config, args.steps, args.warmup)
+    w, qkv, wall, per = run_attention(args.config, args.steps, args.warmup, args.spinup_ms)
     ms = wall * 1e3 / args.steps
     avg_launch_ms = float(np.mean(per))
     flops = w.flops
@@ -185,7 +209,7 @@ def main():
         "metric": METRIC,
         "value": tflops if not decode_bound else w.bytes_qkvo / (ms * 1e-3) / 1e9,
         "unit": "TFLOP/s" if not decode_bound else "GB/s",
-        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "spinup_ms": args.spinup_ms, "ms_per_step": ms,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "Sq": w.Sq, "Sk": w.Sk, "D": w.D,
@@ -194,7 +218,7 @@ def main():
         "roofline": roof,
     }
     if not args.no_decode and args.config != 3:
-        wd, _, wall_d, per_d = run_attention(3, max(5, args.steps // 2), 2)
+        wd, _, wall_d, per_d = run_attention(3, max(5, args.steps // 2), 2, min(args.spinup_ms, 100.0))
         ms_d = float(np.mean(per_d))
         gbs = wd.bytes_qkvo / (ms_d * 1e-3) / 1e9
         out["decode"] = {"workload": wd.name, "ms_per_step": ms_d, "value": gbs, "unit": "GB/s",

@@ -3,15 +3,19 @@
 // state machine as the prefill kernel (Alg. 1 per query row, block-aware
 // rescaling, HiF8 T and P), shaped for the HBM-bound regime:
 //
-//   - one wave per workgroup owns up to 16 flattened (query position, query
-//     head of the group) rows of one key/value head, on 16x16x32 bf16 MFMAs;
-//   - K and V stream through a ring of LDS slots of 32 keys each, filled by
-//     asynchronous global->LDS loads kept R slots ahead.  A single wave needs
-//     no barrier: each slot is consumed after the vector-memory counter says
-//     its loads landed, and refilled after the MFMAs that read it were issued;
-//   - 80 KiB of LDS per workgroup (ring + score table), so two workgroups
-//     share a CU and every (batch, key/value head) stream of a large batch
-//     is in flight at once.
+//   - a workgroup owns up to 16 flattened (query position, query head of the
+//     group) rows of one key/value head, on 16x16x32 bf16 MFMAs;
+//   - its BLK/32 waves split every key block: wave w takes the 32 keys
+//     [32w, 32w + 32) of each block, so the waves stream disjoint parts of
+//     the K/V rows concurrently;
+//   - per block the waves exchange their partial row maxima through LDS (one
+//     barrier) and then all take the same Alg. 1 decision from the same
+//     maximum, so every wave holds the same reference; their output and
+//     denominator partials are therefore on one scale and are summed once at
+//     the end;
+//   - each wave streams its K and V slots through its own LDS ring, filled by
+//     asynchronous global->LDS loads kept RW slots ahead; a slot is consumed
+//     after the vector-memory counter says it landed and refilled right after.
 #include "common.hpp"
 
 namespace baps {
@@ -27,14 +31,18 @@ __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast
 constexpr int kRows = 16;            // query rows per workgroup
 constexpr int kSlotKeys = 32;        // keys per ring slot
 
-template <int D>
+template <int D, int BLK>
 struct DCfg {
+    static constexpr int kWaves = BLK / kSlotKeys;              // one wave per 32-key slot of a block
     static constexpr int kRowBytes = 2 * D;
     static constexpr int kCPR = D / 8;                          // 16-byte chunks per row
     static constexpr int kSlotBytes = kSlotKeys * kRowBytes;    // 8 KiB (D=128), 4 KiB (D=64)
     static constexpr int kIPS = kSlotBytes / 1024;              // wave-wide loads per slot
-    static constexpr int kRing = 64 / kIPS;                     // slots; keeps <= 63 loads outstanding
-    static constexpr int kLdsBytes = kRing * kSlotBytes;
+    // ring slots per wave: about 64 KiB of ring per workgroup, at least 2,
+    // and at most 63 loads outstanding per wave
+    static constexpr int kRW0 = (64 * 1024) / (kWaves * kSlotBytes);
+    static constexpr int kRW = kRW0 < 2 ? 2 : (kRW0 * kIPS > 63 ? 63 / kIPS : kRW0);
+    static constexpr int kLdsBytes = kWaves * kRW * kSlotBytes;
 };
 
 // chunk swizzles (same bank-conflict reasoning as the prefill kernel): K rows
@@ -44,9 +52,11 @@ __device__ __forceinline__ int k_swz(int r) { return D == 128 ? (r & 15) : ((r >
 template <int D>
 __device__ __forceinline__ int v_swz(int r) { return D == 128 ? 2 * (r & 3) : 2 * ((r >> 1) & 1); }
 
+// One wave-wide asynchronous global->LDS load of 1 KiB, marked non-temporal:
+// every K/V byte is read once, so the stream should not displace cached data
 __device__ __forceinline__ void lds_dma_16(const void* gptr, uint32_t lds_base)
 {
-    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off nt"
                  :
                  : "v"(gptr), "s"(lds_base)
                  : "memory", "m0");
@@ -63,22 +73,28 @@ __device__ __forceinline__ void wait_vm(int n)
     }
 }
 
-template <int D, int BLK>
-__global__ __launch_bounds__(64) void baps_attn_decode_kernel(AttnParams p)
+template <int D, int BLK, bool CT>
+__global__ __launch_bounds__(64 * (BLK / 32)) void baps_attn_decode_kernel(AttnParams p)
 {
     static_assert(D == 64 || D == 128, "head dimension");
     static_assert(BLK % kSlotKeys == 0 && BLK <= 128, "key block");
-    using C = DCfg<D>;
-    __shared__ __attribute__((aligned(16))) uint16_t tab[kTabEntries];
+    using C = DCfg<D, BLK>;
+    constexpr int KW = C::kWaves;
+    constexpr int RW = C::kRW;
+    // P lookup: the compact code table (lambda <= kCodeMaxLambda), else the
+    // bf16 half of the full score table
+    __shared__ __attribute__((aligned(16))) uint8_t ctab[CT ? kCodeHi + 1 : 1];
+    __shared__ __attribute__((aligned(16))) uint16_t tab[CT ? 1 : kTabEntries];
+    __shared__ float xch[2][KW][kRows];           // partial row maxima, by block parity
     extern __shared__ __attribute__((aligned(1024))) char ring[];
     const uint32_t ring_lds = (uint32_t)(uintptr_t)LDS_PTR(char, ring);
 
-    constexpr int kSPB = BLK / kSlotKeys;        // K (and V) slots per block
-    constexpr int kKT = BLK / 16;                 // 16-key S^T tiles per block
     constexpr int kDK = D / 32;                   // 32-wide d chunks (QK^T contraction)
     constexpr int kDT = D / 16;                   // 16-wide d tiles of O^T
 
-    const int lane = threadIdx.x;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int c16 = lane & 15;                    // query column of this lane
     const int grp = lane >> 4;                    // lane group 0..3
 
@@ -94,16 +110,17 @@ __global__ __launch_bounds__(64) void baps_attn_decode_kernel(AttnParams p)
     const int f_last = min(flat_rows - 1, tile * kRows + kRows - 1);
     const int kmax_tile = p.causal ? min(p.Sk - 1, f_last / G + off) : p.Sk - 1;
     const int nblk = kmax_tile < 0 ? 0 : kmax_tile / BLK + 1;
-    const int nslots = 2 * kSPB * nblk;           // K slots then V slots, block by block
+    const int nslots = 2 * nblk;                  // this wave's slots: K then V of each block
 
-    // slot n: block n / (2 kSPB); within the block K slots first, then V
+    // slot n of this wave: block n/2, keys 32*wave .. +32 of the block; K if n is even
+    const uint32_t my_ring_lds = ring_lds + (uint32_t)(wave * RW * C::kSlotBytes);
+    const char* my_ring = ring + wave * RW * C::kSlotBytes;
     auto issue_slot = [&](int n) {
-        const int jb = n / (2 * kSPB);
-        const int w = n % (2 * kSPB);
-        const bool is_v = w >= kSPB;
-        const int key0 = jb * BLK + (w % kSPB) * kSlotKeys;
+        const int jb = n >> 1;
+        const bool is_v = (n & 1) != 0;
+        const int key0 = jb * BLK + wave * kSlotKeys;
         const uint16_t* base = is_v ? vbase : kbase;
-        const uint32_t dst = ring_lds + (uint32_t)((n % C::kRing) * C::kSlotBytes);
+        const uint32_t dst = my_ring_lds + (uint32_t)((n % RW) * C::kSlotBytes);
 #pragma unroll
         for (int t = 0; t < C::kIPS; ++t) {
             const int r = t * (1024 / C::kRowBytes) + lane / C::kCPR;
@@ -114,9 +131,13 @@ __global__ __launch_bounds__(64) void baps_attn_decode_kernel(AttnParams p)
         }
     };
     int issued = 0;
-    for (; issued < min(nslots, C::kRing); ++issued) issue_slot(issued);
+    for (; issued < min(nslots, RW); ++issued) issue_slot(issued);
 
-    for (int i = lane; i < kTabEntries; i += 64) tab[i] = (uint16_t)(p.tab[i] >> 16);
+    if constexpr (CT) {
+        for (int i = tid; i < kCodeEntries; i += 64 * KW) ctab[kCodeLo + i] = p.ctab[i];
+    } else {
+        for (int i = tid; i < kTabEntries; i += 64 * KW) tab[i] = (uint16_t)(p.tab[i] >> 16);
+    }
 
     // this lane's query row
     const int f = tile * kRows + c16;
@@ -142,38 +163,37 @@ __global__ __launch_bounds__(64) void baps_attn_decode_kernel(AttnParams p)
     const float ninf = -__builtin_huge_valf();
     const float c = p.c;
     const float lam = (float)p.lambda;
-    // Alg. 1 state; output and denominator kept relative to the current
-    // block reference (one exact rescale when the reference moves)
+    // Alg. 1 state (the same in every wave); output and denominator partials
+    // kept relative to the current block reference
     float m = ninf, ref = ninf, dl = 0.0f;
     unsigned n_restart = 0, n_visit = 0;
     f32x4 oacc[kDT];
 #pragma unroll
     for (int t = 0; t < kDT; ++t) oacc[t] = f32x4{};
 
-    const int kx = k_swz<D>(c16);                 // K rows 16*kt + c16
+    const int kx = k_swz<D>(c16);                 // K rows 16*t2 + c16
     const uint32_t krow = c16 * C::kRowBytes;
-    const int vrow0 = 4 * grp + c16 / 4;          // + 32*slot row offsets, +16 for slots 4..7
+    const int vrow0 = 4 * grp + c16 / 4;          // +16 for slots 4..7
     const int vx = v_swz<D>(vrow0);
     const int vd0 = 4 * (c16 & 3);                // + 16*dt
     const uint32_t vrow = vrow0 * C::kRowBytes + 2 * (vd0 & 7);
 
     int consumed = 0;
-    auto wait_slot = [&](int n) {                 // slot n has landed in LDS
-        wait_vm((issued - 1 - n) * C::kIPS);
-    };
-    auto next_slot = [&]() {                      // the slot just read is refilled
+    auto wait_slot = [&](int n) { wait_vm((issued - 1 - n) * C::kIPS); };
+    auto next_slot = [&]() {
         if (issued < nslots) { issue_slot(issued); ++issued; }
         ++consumed;
     };
+    __syncthreads();                              // code table published
 
+    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
     for (int jb = 0; jb < nblk; ++jb) {
-        const int key0 = jb * BLK;
-        // S^T = K_j Q^T, 16 keys per tile, two tiles per slot
-        f32x4 sacc[kKT];
-#pragma unroll
-        for (int s = 0; s < kSPB; ++s) {
+        const int key0 = jb * BLK + wave * kSlotKeys;   // this wave's first key of the block
+        // S^T = K Q^T for this wave's 32 keys: two 16-key tiles
+        f32x4 sacc[2];
+        {
             wait_slot(consumed);
-            const char* slot = ring + (consumed % C::kRing) * C::kSlotBytes;
+            const char* slot = my_ring + (consumed % RW) * C::kSlotBytes;
 #pragma unroll
             for (int t2 = 0; t2 < 2; ++t2) {
                 f32x4 acc = {};
@@ -183,27 +203,34 @@ __global__ __launch_bounds__(64) void baps_attn_decode_kernel(AttnParams p)
                         slot + krow + t2 * 16 * C::kRowBytes + 16 * ((4 * kk + grp) ^ kx));
                     acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a), as_bf16x8(qop[kk]), acc, 0, 0, 0);
                 }
-                sacc[2 * s + t2] = acc;
+                sacc[t2] = acc;
             }
             next_slot();
         }
-        // mask keys past kmax; register i of tile kt holds key key0 + 16*kt + 4*grp + i
-        if (key0 + BLK - 1 > kmax_lo) {
+        // mask keys past kmax; register i of tile t2 holds key key0 + 16*t2 + 4*grp + i
+        if (key0 + kSlotKeys - 1 > kmax_lo) {
             asm volatile("" ::: "memory");
             const int lim = kmax - key0 - 4 * grp;
 #pragma unroll
-            for (int kt = 0; kt < kKT; ++kt)
+            for (int t2 = 0; t2 < 2; ++t2)
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
-                    if (16 * kt + i > lim) sacc[kt][i] = ninf;
+                    if (16 * t2 + i > lim) sacc[t2][i] = ninf;
         }
-        float amax = ninf;
+        // row maximum of the block: this wave's 32 keys, then across the waves
+        float pm = __builtin_fmaxf(__builtin_fmaxf(__builtin_fmaxf(sacc[0][0], sacc[0][1]), sacc[0][2]),
+                                   __builtin_fmaxf(__builtin_fmaxf(sacc[0][3], sacc[1][0]), sacc[1][1]));
+        pm = __builtin_fmaxf(pm, __builtin_fmaxf(sacc[1][2], sacc[1][3]));
+        pm = __builtin_fmaxf(pm, __shfl_xor(pm, 16, 64));
+        pm = __builtin_fmaxf(pm, __shfl_xor(pm, 32, 64));
+        float amax = pm;
+        if constexpr (KW > 1) {
+            if (grp == 0) xch[jb & 1][wave][c16] = pm;
+            __syncthreads();
+            amax = xch[jb & 1][0][c16];
 #pragma unroll
-        for (int kt = 0; kt < kKT; ++kt)
-            amax = __builtin_fmaxf(amax, __builtin_fmaxf(__builtin_fmaxf(sacc[kt][0], sacc[kt][1]),
-                                                         __builtin_fmaxf(sacc[kt][2], sacc[kt][3])));
-        amax = __builtin_fmaxf(amax, __shfl_xor(amax, 16, 64));
-        amax = __builtin_fmaxf(amax, __shfl_xor(amax, 32, 64));
+            for (int w = 1; w < KW; ++w) amax = __builtin_fmaxf(amax, xch[jb & 1][w][c16]);
+        }
 
         // block-aware precision rescaling (Alg. 1), per row (see the prefill kernel)
         const bool vis = amax != ninf;
@@ -228,26 +255,29 @@ __global__ __launch_bounds__(64) void baps_attn_decode_kernel(AttnParams p)
         ref = ref_new;
         const float nref = (ref == ninf) ? 0.0f : -ref;
 
-        // P = HiF8(2^HiF8(T)); a 32-key chunk (tiles 2s, 2s+1) forms one B
-        // operand: slots 0..3 = keys 4*grp + i, slots 4..7 = keys 16 + 4*grp + i
-        const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+        // P = HiF8(2^HiF8(T)) of the 32 keys as one B operand: slots 0..3 =
+        // keys 4*grp + i, slots 4..7 = keys 16 + 4*grp + i
+        u32x4 pop;
 #pragma unroll
-        for (int s = 0; s < kSPB; ++s) {
-            u32x4 pop;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int kt = 2 * s + (e >> 1);
-                const float t0 = __builtin_fmaf(sacc[kt][2 * (e & 1)], c, nref);
-                const float t1 = __builtin_fmaf(sacc[kt][2 * (e & 1) + 1], c, nref);
-                const uint32_t p0 = tab[hif8::f2u(t0) >> kTabShift];
-                const uint32_t p1 = tab[hif8::f2u(t1) >> kTabShift];
-                const uint32_t w = p0 | (p1 << 16);
-                pop[e] = w;
-                dl = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), ones, dl, false);
+        for (int e = 0; e < 4; ++e) {
+            const int t2 = e >> 1;
+            const float t0 = __builtin_fmaf(sacc[t2][2 * (e & 1)], c, nref);
+            const float t1 = __builtin_fmaf(sacc[t2][2 * (e & 1) + 1], c, nref);
+            uint32_t w;
+            if constexpr (CT) {
+                const uint32_t i0 = min(max(hif8::f2u(t0) >> kTabShift, (uint32_t)kCodeLo), (uint32_t)kCodeHi);
+                const uint32_t i1 = min(max(hif8::f2u(t1) >> kTabShift, (uint32_t)kCodeLo), (uint32_t)kCodeHi);
+                w = ((uint32_t)ctab[i0] | ((uint32_t)ctab[i1] << 16)) << 4;
+            } else {
+                w = (uint32_t)tab[hif8::f2u(t0) >> kTabShift] | ((uint32_t)tab[hif8::f2u(t1) >> kTabShift] << 16);
             }
-            // X^T += V^T P^T for this slot's 32 keys
+            pop[e] = w;
+            dl = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), ones, dl, false);
+        }
+        // X^T += V^T P^T for these 32 keys
+        {
             wait_slot(consumed);
-            const char* slot = ring + (consumed % C::kRing) * C::kSlotBytes;
+            const char* slot = my_ring + (consumed % RW) * C::kSlotBytes;
 #pragma unroll
             for (int t = 0; t < kDT; ++t) {
                 const char* pa = slot + vrow + 16 * (((16 * t + vd0) >> 3) ^ vx);
@@ -261,14 +291,39 @@ __global__ __launch_bounds__(64) void baps_attn_decode_kernel(AttnParams p)
         }
     }
 
-    // epilogue: O = X / dX, lse = ln2 (ref + log2 dX); the 4 lanes of a
-    // query hold disjoint d rows 16*t + 4*grp + i
-    float d = dl + __shfl_xor(dl, 16, 64);
-    d += __shfl_xor(d, 32, 64);
+    // sum the waves' partials (one reference scale) through the ring, then
+    // O = X / dX, lse = ln2 (ref + log2 dX); the 4 lanes of a query hold
+    // disjoint d rows 16*t + 4*grp + i
+    float dw = dl + __shfl_xor(dl, 16, 64);
+    dw += __shfl_xor(dw, 32, 64);
+    if constexpr (KW > 1) {
+        float* mb = reinterpret_cast<float*>(ring);             // [KW-1][kRows][D]
+        float* db = mb + (KW - 1) * kRows * D;                  // [KW-1][kRows]
+        __syncthreads();                                        // every wave is done with its ring
+        if (wave > 0) {
+            float* mine = mb + (wave - 1) * kRows * D + c16 * D;
+#pragma unroll
+            for (int t = 0; t < kDT; ++t) *reinterpret_cast<f32x4*>(mine + 16 * t + 4 * grp) = oacc[t];
+            if (grp == 0) db[(wave - 1) * kRows + c16] = dw;
+        }
+        __syncthreads();
+        if (wave > 0) return;
+#pragma unroll
+        for (int w = 1; w < KW; ++w) {
+            const float* theirs = mb + (w - 1) * kRows * D + c16 * D;
+#pragma unroll
+            for (int t = 0; t < kDT; ++t) {
+                const f32x4 v = *reinterpret_cast<const f32x4*>(theirs + 16 * t + 4 * grp);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) oacc[t][e] += v[e];
+            }
+            dw += db[(w - 1) * kRows + c16];
+        }
+    }
     if (!row_ok) return;
     float* orow = p.o + (((long long)b * p.Hq + h) * p.Sq + r) * D;
     const bool empty = (ref == ninf);
-    const float inv = empty ? 0.0f : 1.0f / d;
+    const float inv = empty ? 0.0f : 1.0f / dw;
 #pragma unroll
     for (int t = 0; t < kDT; ++t) {
         f32x4 v;
@@ -277,7 +332,8 @@ __global__ __launch_bounds__(64) void baps_attn_decode_kernel(AttnParams p)
         *reinterpret_cast<f32x4*>(orow + 16 * t + 4 * grp) = v;
     }
     if (grp == 0) {
-        if (p.lse) p.lse[((long long)b * p.Hq + h) * p.Sq + r] = empty ? ninf : 0.69314718055994531f * (ref + log2f(d));
+        const float dbias = CT ? (float)kCodeBiasLog2 : 0.0f;
+        if (p.lse) p.lse[((long long)b * p.Hq + h) * p.Sq + r] = empty ? ninf : 0.69314718055994531f * (ref + (log2f(dw) + dbias));
         if (p.counters && n_visit) {
             atomicAdd(p.counters + 2 * ((long long)b * p.Hq + h) + 0, (unsigned long long)n_restart);
             atomicAdd(p.counters + 2 * ((long long)b * p.Hq + h) + 1, (unsigned long long)n_visit);
@@ -285,33 +341,41 @@ __global__ __launch_bounds__(64) void baps_attn_decode_kernel(AttnParams p)
     }
 }
 
-template <int D, int BLK>
+template <int D, int BLK, bool CT>
 hipError_t launch_dec(const AttnParams& p, hipStream_t st)
 {
-    using C = DCfg<D>;
+    using C = DCfg<D, BLK>;
+    static_assert(C::kLdsBytes >= (C::kWaves - 1) * kRows * (D + 1) * 4, "merge buffer fits the ring");
     static bool attr_set = false;
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&baps_attn_decode_kernel<D, BLK>),
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&baps_attn_decode_kernel<D, BLK, CT>),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, C::kLdsBytes);
         if (e != hipSuccess) return e;
         attr_set = true;
     }
     const long long flat = (long long)p.Sq * (p.Hq / p.Hkv);
     const dim3 grid((unsigned)((flat + kRows - 1) / kRows), (unsigned)p.Hkv, (unsigned)p.B);
-    hipLaunchKernelGGL((baps_attn_decode_kernel<D, BLK>), grid, dim3(64), C::kLdsBytes, st, p);
+    hipLaunchKernelGGL((baps_attn_decode_kernel<D, BLK, CT>), grid, dim3(64 * C::kWaves), C::kLdsBytes, st, p);
     return hipGetLastError();
+}
+
+template <int D, int BLK>
+hipError_t launch_dec_ct(const AttnParams& p, hipStream_t st)
+{
+    if (p.lambda <= kCodeMaxLambda) return launch_dec<D, BLK, true>(p, st);
+    return launch_dec<D, BLK, false>(p, st);
 }
 
 }  // namespace
 
 hipError_t launch_attention_decode(const AttnParams& p, int D, int block, hipStream_t st)
 {
-    if (D == 64 && block == 32) return launch_dec<64, 32>(p, st);
-    if (D == 64 && block == 64) return launch_dec<64, 64>(p, st);
-    if (D == 64 && block == 128) return launch_dec<64, 128>(p, st);
-    if (D == 128 && block == 32) return launch_dec<128, 32>(p, st);
-    if (D == 128 && block == 64) return launch_dec<128, 64>(p, st);
-    if (D == 128 && block == 128) return launch_dec<128, 128>(p, st);
+    if (D == 64 && block == 32) return launch_dec_ct<64, 32>(p, st);
+    if (D == 64 && block == 64) return launch_dec_ct<64, 64>(p, st);
+    if (D == 64 && block == 128) return launch_dec_ct<64, 128>(p, st);
+    if (D == 128 && block == 32) return launch_dec_ct<128, 32>(p, st);
+    if (D == 128 && block == 64) return launch_dec_ct<128, 64>(p, st);
+    if (D == 128 && block == 128) return launch_dec_ct<128, 128>(p, st);
     return hipErrorInvalidValue;
 }
 
