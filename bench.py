@@ -108,6 +108,32 @@ def run_attention(cfg, steps, warmup, spinup_ms=0.0):
     return w, (q, k, v), wall, per
 
 
+def softmax_setups(cfg, steps=20):
+    """The same workload through the two eq. (2) setups on the same tiling
+    (Default: fp32 softmax; Exp2 HiF8: 8-bit exp2 with the real-valued max),
+    for the in-house cost of the 8-bit softmax.  Per-launch mean, in
+    algorithmic TFLOP/s."""
+    import torch
+    import paper_2602_02071_amd as baps
+    from paper_2602_02071_amd.workloads import make_workload
+    w, q, k, v = make_workload(cfg)
+    dev = torch.device("cuda:0")
+    qt, kt, vt = (torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).to(dev) for x in (q, k, v))
+    o = torch.empty((w.B, w.Hq, w.Sq, w.D), dtype=torch.float32, device=dev)
+    lse = torch.empty((w.B, w.Hq, w.Sq), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream().cuda_stream
+    res = {}
+    for name, mode in (("default", baps.BAPS_MODE_DEFAULT), ("exp2_hif8", baps.BAPS_MODE_EXP2_HIF8),
+                       ("e2e_hif8", baps.BAPS_MODE_E2E_HIF8)):
+        def step():
+            baps.baps_attention_fwd_ex(qt, kt, vt, o, lse, w.B, w.Hq, w.Hkv, w.Sq, w.Sk, w.D, w.causal, w.block,
+                                       stream=stream, mode=mode)
+        _, per = _time_launches(step, steps, 3, 50.0)
+        ms = float(np.mean(per))
+        res[name] = {"us": ms * 1e3, "TFLOP/s": w.flops / (ms * 1e-3) / 1e12}
+    return res
+
+
 def boundary_kernels(steps=10):
     """Throughput of the standalone boundary kernels on HBM-sized inputs:
     hif8_encode / hif8_decode over 2^28 elements (1 GiB of fp32, beyond the
@@ -182,6 +208,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-boundary", action="store_true", help="skip the codec / softmax-block kernels")
+    ap.add_argument("--no-modes", action="store_true", help="skip the Default / Exp2 HiF8 comparison")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -225,6 +252,8 @@ def main():
                          "tokens_per_s": wd.B / (ms_d * 1e-3),
                          "roofline": {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                                       "frac": gbs / PEAK_HBM_GBS, "traffic": _traffic("attn_fwd_decode")}}
+    if not args.no_modes and w.Sq > 1:
+        out["softmax_setups"] = softmax_setups(args.config)
     if not args.no_boundary:
         out["boundary"] = boundary_kernels()
     if not args.no_cpu_baseline:

@@ -61,6 +61,20 @@ int baps_attention_fwd(const void* q, const void* k, const void* v, float* o, fl
                        int B, int Hq, int Hkv, int Sq, int Sk, int D, int causal, int block,
                        void* stream);
 
+/* Softmax setups (Sec. 4.1, Table 1).  BAPS_MODE_E2E_HIF8 is the proposed
+ * workflow (Alg. 1).  The two others follow eq. (2) with the real-valued
+ * running maximum m, on the same tiling, for comparison:
+ *   BAPS_MODE_DEFAULT    every softmax operation in fp32: P = 2^fl32(S - m),
+ *                        rescale 2^(m_old - m); P enters P V rounded to bf16,
+ *                        the denominator sums the fp32 P;
+ *   BAPS_MODE_EXP2_HIF8  the exp2 on 8-bit input, rounded to 8 bits:
+ *                        P = HiF8(2^HiF8(fl32(S - m))), likewise the rescale
+ *                        factor; S = fl32(fl32(q.k) * scale).
+ * lambda, n_b0 and restart_counts apply to BAPS_MODE_E2E_HIF8 only. */
+#define BAPS_MODE_E2E_HIF8 0
+#define BAPS_MODE_DEFAULT 1
+#define BAPS_MODE_EXP2_HIF8 2
+
 /* Knobs of Alg. 1 and the paper's ablations (Sec. 4.1, Table 4). */
 typedef struct {
     int lambda;                          /* restart threshold (integer, Alg. 1); 1 canonical  */
@@ -69,6 +83,7 @@ typedef struct {
     unsigned long long* restart_counts;  /* device [B*Hq][2]: restarted and visited B1 row-
                                             blocks (accumulated with atomics; the caller
                                             zeroes it); NULL to skip                          */
+    int mode;                            /* BAPS_MODE_*; anything else is an invalid argument  */
 } baps_params_t;
 
 /* baps_attention_fwd with explicit knobs; p must not be NULL; scale_log2

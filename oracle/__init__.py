@@ -86,7 +86,7 @@ def _load():
                                 i32, i32, i32, i32, d, P, i64, P, P, P, i32]
     L.orc_attention_ex.restype = i32
     L.orc_attention_ex.argtypes = [P, P, P, i32, i32, i32, i32, i32, i32, i32, i32,
-                                   i32, i32, i32, i32, d, P, i64, P, P, P, P, d, ctypes.c_uint64, i32]
+                                   i32, i32, i32, i32, d, P, i64, P, P, P, P, d, ctypes.c_uint64, i32, i32]
     L.orc_exact_attention.restype = i32
     L.orc_exact_attention.argtypes = [P, P, P, i32, i32, i32, i32, i32, i32, i32,
                                       d, P, i64, P, P, i32]
@@ -189,7 +189,7 @@ def _rows(rows, total):
 
 def attention(q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, block, mode=E2E_HIF8, lam=1, n_b0=1,
               literal_else=False, scale_log2=0.0, rows=None, nthreads=0, margin=False, jitter=0.0,
-              jitter_seed=0):
+              jitter_seed=0, pv_bf16=False):
     """Attention rows in one of the paper's setups.
 
     q: [B,Hq,Sq,D], k/v: [B,Hkv,Sk,D] bf16 bit patterns.  rows: global row
@@ -199,7 +199,10 @@ def attention(q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, block, mode=E2E_HIF8, lam=
     decisions sit from a rounding boundary, in units of the fp32 dot-product
     accumulation error bound (>= 1: every valid high-precision S yields this
     result).  jitter moves every dot product by jitter times that bound
-    (same direction for jitter_seed 0, random signs otherwise)."""
+    (same direction for jitter_seed 0, random signs otherwise).  pv_bf16 (the
+    setups of eq. (2) only): P enters the P V product rounded to bf16, the
+    input precision of a matrix unit, while the denominator sums P as
+    computed."""
     L = _load()
     q, k, v = _bits(q), _bits(k), _bits(v)
     rows = _rows(rows, B * Hq * Sq)
@@ -211,7 +214,7 @@ def attention(q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, block, mode=E2E_HIF8, lam=
     st = L.orc_attention_ex(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, Sq, Sk, D, int(causal), block,
                             int(mode), int(lam), int(n_b0), int(literal_else), float(scale_log2),
                             _ptr(rows), n, _ptr(o), _ptr(lse), _ptr(nrs), _ptr(mg), float(jitter),
-                            ctypes.c_uint64(int(jitter_seed)), int(nthreads))
+                            ctypes.c_uint64(int(jitter_seed)), int(nthreads), int(bool(pv_bf16)))
     if st:
         raise ValueError("oracle rejected the attention arguments")
     if margin:

@@ -364,6 +364,7 @@ typedef struct {
     double* margin;         /* decision margin per row (nullable), see row_alg1 */
     double jitter;          /* move each dot product by jitter * its error bound */
     uint64_t jitter_seed;   /* 0: every dot product moves the same way; else random signs */
+    int pv_bf16;            /* eq. (2) setups: P enters the P V product rounded to bf16 */
 } attn_job;
 
 static inline double bf16_to_double(uint16_t b)
@@ -579,7 +580,19 @@ static void row_alg1(const attn_job* J, int b, int h, int r, row_scratch* W,
 /* One query row of eq. (2) in the setups of Sec. 4.1 / Table 1 that keep the
  * real-valued running maximum: Default, Exp2 HiF8, Naive E2E, Exp2 FP8.
  * The softmax runs in fp32 as the Default setup states. */
-static void row_eq2(const attn_job* J, int b, int h, int r, row_scratch* W, double* o, double* lse)
+/* p rounded to bf16 (to nearest, ties to even): the precision of the matrix
+ * unit's inputs, at which P enters the P V product (pv_bf16) */
+static float round_bf16(float p)
+{
+    uint32_t u;
+    memcpy(&u, &p, 4);
+    u = (u + 0x7FFFu + ((u >> 16) & 1u)) & 0xFFFF0000u;
+    memcpy(&p, &u, 4);
+    return p;
+}
+
+static void row_eq2(const attn_job* J, int b, int h, int r, row_scratch* W, double* o, double* lse,
+                    double* margin_out)
 {
     const int D = J->D, blk = J->block;
     const int g = h / (J->Hq / J->Hkv);
@@ -588,11 +601,17 @@ static void row_eq2(const attn_job* J, int b, int h, int r, row_scratch* W, doub
     const uint16_t* vb = J->v + ((int64_t)b * J->Hkv + g) * (int64_t)J->Sk * D;
     const int kmax = last_visible_key(J, r);
     const int nblk = kmax < 0 ? 0 : kmax / blk + 1;
+    const uint64_t rowid = (((uint64_t)b * J->Hq + h) * J->Sq + r);
     const orc_format *fin = &F_HIF8, *fout = &F_HIF8;
     if (J->mode == ORC_EXP2_E4M3) { fin = &F_E4M3; fout = &F_E4M3; }
     if (J->mode == ORC_EXP2_E5M2) { fin = &F_E5M2; fout = &F_E5M2; }
     if (J->mode == ORC_EXP2_E4M3xE5M2) { fin = &F_E4M3; fout = &F_E5M2; }
+    /* the decisions whose margin is reported: the HiF8 roundings of the Exp2
+     * HiF8 setup, and with pv_bf16 the bf16 roundings of P in Default */
+    const int hif8_dec = (J->mode == ORC_EXP2_HIF8);
     float m = -INFINITY, d = 0.0f;
+    double eps_m = 0.0;                                                  /* error bound of m, in S units */
+    double mg = INFINITY;
     float* ot = (float*)W->pv;                                           /* fp32 O~ */
     for (int i = 0; i < D; ++i) ot[i] = 0.0f;
 
@@ -601,17 +620,36 @@ static void row_eq2(const attn_job* J, int b, int h, int r, row_scratch* W, doub
         const int c1 = (c0 + blk <= kmax + 1) ? c0 + blk : kmax + 1;
         const int nc = c1 - c0;
         float rowmax = -INFINITY;
+        double eps_rowmax = 0.0;
         for (int c = 0; c < nc; ++c) {
-            float s = (float)dot64(qr, kb + (int64_t)(c0 + c) * D, D) * J->c32;
+            const uint16_t* kr = kb + (int64_t)(c0 + c) * D;
+            double a = dot64(qr, kr, D);
+            const double e_acc = ACC_ERR * ldexp(abs_dot64(qr, kr, D), -24);
+            if (J->jitter != 0.0) {
+                double sgn = 1.0;
+                if (J->jitter_seed)
+                    sgn = (splitmix64(J->jitter_seed ^ (rowid * 1000003ull + (uint64_t)(c0 + c))) & 1) ? 1.0 : -1.0;
+                a += J->jitter * sgn * e_acc;
+            }
+            float s = (float)a * J->c32;                                 /* S = fl32(fl32(q.k) * c) */
             if (J->mode == ORC_NAIVE_E2E) s = (float)fmt_round(&F_HIF8, s, 1);   /* scores cast first */
             W->acc[c] = s;
-            if (s > rowmax) rowmax = s;
+            W->eps[c] = e_acc * J->c64;
+            if (s > rowmax) { rowmax = s; eps_rowmax = W->eps[c]; }
         }
         const float m_new = m > rowmax ? m : rowmax;                     /* m^(j) */
+        const double eps_new = m > rowmax ? eps_m : eps_rowmax;
         float alpha;
         if (m == -INFINITY) alpha = 0.0f;
         else if (J->mode == ORC_DEFAULT) alpha = exp2f(m - m_new);
-        else alpha = (float)fmt_round(fout, exp2(fmt_round(fin, (double)(m - m_new), 1)), 1);
+        else {
+            const float x = m - m_new;
+            alpha = (float)fmt_round(fout, exp2(fmt_round(fin, (double)x, 1)), 1);
+            if (hif8_dec && m_new != m) {
+                const double dist = hif8_boundary_distance((double)x) / (eps_m + eps_new);
+                if (dist < mg) mg = dist;
+            }
+        }
         float rowsum = 0.0f;
         d *= alpha;
         for (int i = 0; i < D; ++i) ot[i] *= alpha;
@@ -619,14 +657,38 @@ static void row_eq2(const attn_job* J, int b, int h, int r, row_scratch* W, doub
             float x = (float)W->acc[c] - m_new;
             float p;
             if (J->mode == ORC_DEFAULT) p = exp2f(x);
-            else p = (float)fmt_round(fout, exp2(fmt_round(fin, (double)x, 1)), 1);
+            else {
+                p = (float)fmt_round(fout, exp2(fmt_round(fin, (double)x, 1)), 1);
+                /* a score carrying weight >= 2^-12 of the block maximum's whose
+                 * rounding sits near a boundary */
+                if (hif8_dec && x > -12.0f && W->acc[c] != m_new) {
+                    const double dist = hif8_boundary_distance((double)x) / (W->eps[c] + eps_new);
+                    if (dist < mg) mg = dist;
+                }
+            }
+            /* with pv_bf16, the bf16 rounding of a weighted P is a decision too:
+             * its distance to the nearest bf16 midpoint against the change of
+             * P that the score error bounds allow (and a few ulps of exp2) */
+            if (J->pv_bf16 && J->mode == ORC_DEFAULT && x > -12.0f && p > 0.0f) {
+                uint32_t u;
+                memcpy(&u, &p, 4);
+                const uint32_t mu = (u & 0xFFFF0000u) | 0x8000u;
+                float mid;
+                memcpy(&mid, &mu, 4);
+                const double dp = (double)p * (M_LN2 * (W->eps[c] + eps_new) + ldexp(1.0, -21));
+                const double dist = fabs((double)p - (double)mid) / dp;
+                if (dist < mg) mg = dist;
+            }
             rowsum += p;
+            const float pv = J->pv_bf16 ? round_bf16(p) : p;
             const uint16_t* vr = vb + (int64_t)(c0 + c) * D;
-            for (int i = 0; i < D; ++i) ot[i] += p * (float)bf16_to_double(vr[i]);
+            for (int i = 0; i < D; ++i) ot[i] += pv * (float)bf16_to_double(vr[i]);
         }
         d += rowsum;
         m = m_new;
+        eps_m = eps_new;
     }
+    if (margin_out) *margin_out = mg;
     if (nblk == 0) {
         for (int i = 0; i < D; ++i) o[i] = 0.0;
         *lse = -INFINITY;
@@ -696,7 +758,7 @@ static void attn_range(void* p, int64_t i0, int64_t i1)
         else if (J->mode == ORC_E2E_HIF8 || J->mode == ORC_E2E_EXACT)
             row_alg1(J, b, h, r, &W, o, lse, J->nrestart ? J->nrestart + i : NULL,
                      J->margin ? J->margin + i : NULL);
-        else row_eq2(J, b, h, r, &W, o, lse);
+        else row_eq2(J, b, h, r, &W, o, lse, J->margin ? J->margin + i : NULL);
     }
     free(W.acc); free(W.eps); free(W.ot); free(W.pv); free(W.ref); free(W.bmargin);
 }
@@ -718,11 +780,11 @@ int orc_attention_ex(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                      int B, int Hq, int Hkv, int Sq, int Sk, int D, int causal, int block,
                      int mode, int lambda, int n_b0, int literal_else, double scale_log2,
                      const int64_t* rows, int64_t nrows, double* o, double* lse, int32_t* nrestart,
-                     double* margin, double jitter, uint64_t jitter_seed, int nthreads)
+                     double* margin, double jitter, uint64_t jitter_seed, int nthreads, int pv_bf16)
 {
     if (attn_check(B, Hq, Hkv, Sq, Sk, D, block) || mode < 0 || mode > 7) return 1;
     attn_job J = { q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, block, mode, lambda, n_b0,
-                   literal_else, 0.0f, 0.0, rows, o, lse, nrestart, margin, jitter, jitter_seed };
+                   literal_else, 0.0f, 0.0, rows, o, lse, nrestart, margin, jitter, jitter_seed, pv_bf16 };
     J.c64 = scale_log2 != 0.0 ? scale_log2 : M_LOG2E / sqrt((double)D);
     J.c32 = (float)J.c64;
     if (mode != ORC_E2E_EXACT) J.c64 = (double)J.c32;
@@ -739,7 +801,7 @@ int orc_attention(const uint16_t* q, const uint16_t* k, const uint16_t* v,
 {
     return orc_attention_ex(q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, block, mode, lambda, n_b0,
                             literal_else, scale_log2, rows, nrows, o, lse, nrestart, NULL, 0.0, 0,
-                            nthreads);
+                            nthreads, 0);
 }
 
 int orc_exact_attention(const uint16_t* q, const uint16_t* k, const uint16_t* v,

@@ -33,7 +33,13 @@ class BapsError(RuntimeError):
 
 class baps_params_t(ctypes.Structure):
     _fields_ = [("lambda_", ctypes.c_int), ("n_b0", ctypes.c_int), ("scale_log2", ctypes.c_float),
-                ("restart_counts", ctypes.c_void_p)]
+                ("restart_counts", ctypes.c_void_p), ("mode", ctypes.c_int)]
+
+
+# softmax setups (include/baps.h)
+BAPS_MODE_E2E_HIF8 = 0
+BAPS_MODE_DEFAULT = 1
+BAPS_MODE_EXP2_HIF8 = 2
 
 
 def load():
@@ -94,8 +100,8 @@ def baps_attention_fwd(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, st
 
 
 def baps_attention_fwd_ex(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, lam=1, n_b0=1,
-                          scale_log2=0.0, restart_counts=None, stream=None):
-    prm = baps_params_t(int(lam), int(n_b0), float(scale_log2), _p(restart_counts))
+                          scale_log2=0.0, restart_counts=None, stream=None, mode=BAPS_MODE_E2E_HIF8):
+    prm = baps_params_t(int(lam), int(n_b0), float(scale_log2), _p(restart_counts), int(mode))
     _check("baps_attention_fwd_ex", load().baps_attention_fwd_ex(
         _p(q), _p(k), _p(v), _p(o), _p(lse), B, Hq, Hkv, Sq, Sk, D, int(causal), block,
         ctypes.byref(prm), _stream(stream)))
@@ -128,7 +134,7 @@ def baps_init():
 
 # ------------------------------------------------------------ tensor helpers
 def attention(q, k, v, causal, block, lse=True, lam=None, n_b0=None, scale_log2=0.0, restart_counts=None,
-              stream=None):
+              stream=None, mode=BAPS_MODE_E2E_HIF8):
     """Allocate O (and lse) with torch on q's device and run the fused pass.
     q [B,Hq,Sq,D], k/v [B,Hkv,Sk,D] bf16 CUDA tensors, contiguous."""
     import torch
@@ -139,10 +145,10 @@ def attention(q, k, v, causal, block, lse=True, lam=None, n_b0=None, scale_log2=
             raise ValueError("q, k, v must be contiguous bf16 device tensors")
     o = torch.empty((B, Hq, Sq, D), dtype=torch.float32, device=q.device)
     l = torch.empty((B, Hq, Sq), dtype=torch.float32, device=q.device) if lse else None
-    if lam is None and n_b0 is None and not scale_log2 and restart_counts is None:
+    if lam is None and n_b0 is None and not scale_log2 and restart_counts is None and mode == BAPS_MODE_E2E_HIF8:
         baps_attention_fwd(q, k, v, o, l, B, Hq, Hkv, Sq, Sk, D, causal, block, stream)
     else:
         baps_attention_fwd_ex(q, k, v, o, l, B, Hq, Hkv, Sq, Sk, D, causal, block,
                               1 if lam is None else lam, 1 if n_b0 is None else n_b0, scale_log2,
-                              restart_counts, stream)
+                              restart_counts, stream, mode)
     return o, l

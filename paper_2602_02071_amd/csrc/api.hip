@@ -112,8 +112,10 @@ int status_of(hipError_t e) { return e == hipSuccess ? BAPS_OK : BAPS_HIP_ERROR;
 
 int attention_impl(const void* q, const void* k, const void* v, float* o, float* lse, int B, int Hq,
                    int Hkv, int Sq, int Sk, int D, int causal, int block, int lambda, int n_b0,
-                   float scale_log2, unsigned long long* counters, void* stream)
+                   float scale_log2, unsigned long long* counters, int mode, void* stream)
 {
+    if (mode != BAPS_MODE_E2E_HIF8 && mode != BAPS_MODE_DEFAULT && mode != BAPS_MODE_EXP2_HIF8)
+        return BAPS_INVALID_ARGUMENT;
     if (B < 0 || Hq < 0 || Hkv < 0 || Sq < 0 || Sk < 0 || n_b0 < 0) return BAPS_INVALID_ARGUMENT;
     if (!(scale_log2 >= 0.0f) || std::isinf(scale_log2)) return BAPS_INVALID_ARGUMENT;
     if (B == 0 || Hq == 0 || Sq == 0) return BAPS_OK;
@@ -140,6 +142,7 @@ int attention_impl(const void* q, const void* k, const void* v, float* o, float*
     p.causal = causal ? 1 : 0;
     p.lambda = lambda;
     p.n_b0 = n_b0;
+    p.mode = mode;
     p.c = scale_log2 > 0.0f ? scale_log2 : (float)(1.4426950408889634 / std::sqrt((double)D));
     return status_of(launch_attention(p, D, block, static_cast<hipStream_t>(stream)));
 }
@@ -153,7 +156,7 @@ int baps_attention_fwd(const void* q, const void* k, const void* v, float* o, fl
 {
     try {
         return attention_impl(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, 1, 1, 0.0f, nullptr,
-                              stream);
+                              BAPS_MODE_E2E_HIF8, stream);
     } catch (...) {
         return BAPS_HIP_ERROR;
     }
@@ -166,7 +169,7 @@ int baps_attention_fwd_ex(const void* q, const void* k, const void* v, float* o,
     if (!prm) return BAPS_INVALID_ARGUMENT;
     try {
         return attention_impl(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, prm->lambda, prm->n_b0,
-                              prm->scale_log2, prm->restart_counts, stream);
+                              prm->scale_log2, prm->restart_counts, prm->mode, stream);
     } catch (...) {
         return BAPS_HIP_ERROR;
     }

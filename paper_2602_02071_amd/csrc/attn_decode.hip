@@ -73,9 +73,10 @@ __device__ __forceinline__ void wait_vm(int n)
     }
 }
 
-template <int D, int BLK, bool CT>
+template <int D, int BLK, bool CT, int MODE>
 __global__ __launch_bounds__(64 * (BLK / 32)) void baps_attn_decode_kernel(AttnParams p)
 {
+    static_assert(MODE == kModeE2E || CT, "the eq. (2) setups use the compact table (T <= 0)");
     static_assert(D == 64 || D == 128, "head dimension");
     static_assert(BLK % kSlotKeys == 0 && BLK <= 128, "key block");
     using C = DCfg<D, BLK>;
@@ -133,7 +134,9 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void baps_attn_decode_kernel(AttnP
     int issued = 0;
     for (; issued < min(nslots, RW); ++issued) issue_slot(issued);
 
-    if constexpr (CT) {
+    if constexpr (MODE == kModeDefault) {
+        // fp32 exp2: no table
+    } else if constexpr (CT) {
         for (int i = tid; i < kCodeEntries; i += 64 * KW) ctab[kCodeLo + i] = p.ctab[i];
     } else {
         for (int i = tid; i < kTabEntries; i += 64 * KW) tab[i] = (uint16_t)(p.tab[i] >> 16);
@@ -232,28 +235,55 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void baps_attn_decode_kernel(AttnP
             for (int w = 1; w < KW; ++w) amax = __builtin_fmaxf(amax, xch[jb & 1][w][c16]);
         }
 
-        // block-aware precision rescaling (Alg. 1), per row (see the prefill kernel)
-        const bool vis = amax != ninf;
-        const bool forced = (jb < p.n_b0) || (m == ninf);
-        const float tq = hif8::round(__builtin_fmaf(amax, c, -m));
-        const bool restart = forced || (ceilf(tq) > lam);
-        const float m_hi = __builtin_fmaxf(m, ceilf(amax * c));
-        const float m_new = vis ? (restart ? m_hi : m + __builtin_fmaxf(0.0f, ceilf(tq))) : m;
-        const float ref_new = vis ? (restart ? m_hi : m) : ref;
-        const bool b1 = vis && (jb >= p.n_b0);
-        n_visit += b1 ? 1u : 0u;
-        n_restart += (b1 && restart) ? 1u : 0u;
-        const float fac = (ref == ninf) ? 1.0f : exp2_int(ref - ref_new);
-        if (__any(fac != 1.0f)) {
+        float nref;
+        if constexpr (MODE == kModeE2E) {
+            // block-aware precision rescaling (Alg. 1), per row (see the prefill kernel)
+            const bool vis = amax != ninf;
+            const bool forced = (jb < p.n_b0) || (m == ninf);
+            const float tq = hif8::round(__builtin_fmaf(amax, c, -m));
+            const bool restart = forced || (ceilf(tq) > lam);
+            const float m_hi = __builtin_fmaxf(m, ceilf(amax * c));
+            const float m_new = vis ? (restart ? m_hi : m + __builtin_fmaxf(0.0f, ceilf(tq))) : m;
+            const float ref_new = vis ? (restart ? m_hi : m) : ref;
+            const bool b1 = vis && (jb >= p.n_b0);
+            n_visit += b1 ? 1u : 0u;
+            n_restart += (b1 && restart) ? 1u : 0u;
+            const float fac = (ref == ninf) ? 1.0f : exp2_int(ref - ref_new);
+            if (__any(fac != 1.0f)) {
+    #pragma unroll
+                for (int t = 0; t < kDT; ++t)
+    #pragma unroll
+                    for (int i = 0; i < 4; ++i) oacc[t][i] *= fac;
+            }
+            dl *= fac;
+            m = m_new;
+            ref = ref_new;
+            nref = (ref == ninf) ? 0.0f : -ref;
+        } else {
+            // eq. (2): real-valued running maximum (see the prefill kernel)
+            const bool vis = amax != ninf;
+            const float m_new = vis ? __builtin_fmaxf(m, amax * c) : m;
+            float fac = 1.0f;
+            if (m != ninf) {
+                const float x = m - m_new;
+                if constexpr (MODE == kModeDefault) {
+                    fac = __builtin_amdgcn_exp2f(x);
+                } else {
+                    const uint32_t ix = min(max(hif8::f2u(x) >> kTabShift, (uint32_t)kCodeLo), (uint32_t)kCodeHi);
+                    fac = hif8::u2f((uint32_t)ctab[ix] << 20) * 0x1p104f;
+                }
+            }
+            if (__any(fac != 1.0f)) {
 #pragma unroll
-            for (int t = 0; t < kDT; ++t)
+                for (int t = 0; t < kDT; ++t)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) oacc[t][i] *= fac;
+                    for (int i = 0; i < 4; ++i) oacc[t][i] *= fac;
+            }
+            dl *= fac;
+            m = m_new;
+            ref = m_new;
+            nref = (m == ninf) ? 0.0f : -m;
         }
-        dl *= fac;
-        m = m_new;
-        ref = ref_new;
-        const float nref = (ref == ninf) ? 0.0f : -ref;
 
         // P = HiF8(2^HiF8(T)) of the 32 keys as one B operand: slots 0..3 =
         // keys 4*grp + i, slots 4..7 = keys 16 + 4*grp + i
@@ -261,9 +291,19 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void baps_attn_decode_kernel(AttnP
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const int t2 = e >> 1;
-            const float t0 = __builtin_fmaf(sacc[t2][2 * (e & 1)], c, nref);
-            const float t1 = __builtin_fmaf(sacc[t2][2 * (e & 1) + 1], c, nref);
             uint32_t w;
+            if constexpr (MODE == kModeDefault) {
+                const float p0 = __builtin_amdgcn_exp2f(sacc[t2][2 * (e & 1)] * c + nref);
+                const float p1 = __builtin_amdgcn_exp2f(sacc[t2][2 * (e & 1) + 1] * c + nref);
+                const bf16x2 pb = {(__bf16)p0, (__bf16)p1};
+                pop[e] = __builtin_bit_cast(uint32_t, pb);
+                dl += p0 + p1;
+                continue;
+            }
+            const float t0 = MODE == kModeE2E ? __builtin_fmaf(sacc[t2][2 * (e & 1)], c, nref)
+                                              : sacc[t2][2 * (e & 1)] * c + nref;
+            const float t1 = MODE == kModeE2E ? __builtin_fmaf(sacc[t2][2 * (e & 1) + 1], c, nref)
+                                              : sacc[t2][2 * (e & 1) + 1] * c + nref;
             if constexpr (CT) {
                 const uint32_t i0 = min(max(hif8::f2u(t0) >> kTabShift, (uint32_t)kCodeLo), (uint32_t)kCodeHi);
                 const uint32_t i1 = min(max(hif8::f2u(t1) >> kTabShift, (uint32_t)kCodeLo), (uint32_t)kCodeHi);
@@ -332,7 +372,7 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void baps_attn_decode_kernel(AttnP
         *reinterpret_cast<f32x4*>(orow + 16 * t + 4 * grp) = v;
     }
     if (grp == 0) {
-        const float dbias = CT ? (float)kCodeBiasLog2 : 0.0f;
+        const float dbias = (CT && MODE != kModeDefault) ? (float)kCodeBiasLog2 : 0.0f;
         if (p.lse) p.lse[((long long)b * p.Hq + h) * p.Sq + r] = empty ? ninf : 0.69314718055994531f * (ref + (log2f(dw) + dbias));
         if (p.counters && n_visit) {
             atomicAdd(p.counters + 2 * ((long long)b * p.Hq + h) + 0, (unsigned long long)n_restart);
@@ -341,29 +381,31 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void baps_attn_decode_kernel(AttnP
     }
 }
 
-template <int D, int BLK, bool CT>
+template <int D, int BLK, bool CT, int MODE>
 hipError_t launch_dec(const AttnParams& p, hipStream_t st)
 {
     using C = DCfg<D, BLK>;
     static_assert(C::kLdsBytes >= (C::kWaves - 1) * kRows * (D + 1) * 4, "merge buffer fits the ring");
     static bool attr_set = false;
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&baps_attn_decode_kernel<D, BLK, CT>),
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&baps_attn_decode_kernel<D, BLK, CT, MODE>),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, C::kLdsBytes);
         if (e != hipSuccess) return e;
         attr_set = true;
     }
     const long long flat = (long long)p.Sq * (p.Hq / p.Hkv);
     const dim3 grid((unsigned)((flat + kRows - 1) / kRows), (unsigned)p.Hkv, (unsigned)p.B);
-    hipLaunchKernelGGL((baps_attn_decode_kernel<D, BLK, CT>), grid, dim3(64 * C::kWaves), C::kLdsBytes, st, p);
+    hipLaunchKernelGGL((baps_attn_decode_kernel<D, BLK, CT, MODE>), grid, dim3(64 * C::kWaves), C::kLdsBytes, st, p);
     return hipGetLastError();
 }
 
 template <int D, int BLK>
 hipError_t launch_dec_ct(const AttnParams& p, hipStream_t st)
 {
-    if (p.lambda <= kCodeMaxLambda) return launch_dec<D, BLK, true>(p, st);
-    return launch_dec<D, BLK, false>(p, st);
+    if (p.mode == kModeDefault) return launch_dec<D, BLK, true, kModeDefault>(p, st);
+    if (p.mode == kModeExp2) return launch_dec<D, BLK, true, kModeExp2>(p, st);
+    if (p.lambda <= kCodeMaxLambda) return launch_dec<D, BLK, true, kModeE2E>(p, st);
+    return launch_dec<D, BLK, false, kModeE2E>(p, st);
 }
 
 }  // namespace

@@ -124,9 +124,10 @@ __device__ __forceinline__ void load_tile(const uint16_t* base, int key0, int Sk
     }
 }
 
-template <int D, int BLK, int NW, bool CT>
+template <int D, int BLK, int NW, bool CT, int MODE>
 __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
 {
+    static_assert(MODE == kModeE2E || CT, "the eq. (2) setups use the compact table (T <= 0)");
     static_assert(D == 64 || D == 128, "head dimension");
     static_assert(BLK % 32 == 0 && BLK <= 128, "key block");
     using C = Cfg<D, BLK, NW>;
@@ -187,7 +188,9 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
         load_tile<D, BLK, NW, false>(kbase, 0, p.Sk, tiles_lds, wave, lane);
         load_tile<D, BLK, NW, true>(vbase, 0, p.Sk, tiles_lds + C::kTileBytes, wave, lane);
     }
-    if constexpr (CT) {
+    if constexpr (MODE == kModeDefault) {
+        // fp32 exp2: no table
+    } else if constexpr (CT) {
         for (int i = tid; i < kCodeEntries; i += C::kThreads) ctab[kCodeLo + i] = p.ctab[i];
     } else {
         for (int i = tid; i < kTabEntries; i += C::kThreads) tab[i] = (uint16_t)(p.tab[i] >> 16);
@@ -312,35 +315,64 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
             amax = __builtin_fmaxf(amax, swap_halves(amax));
         }
 
-        // block-aware precision rescaling (Alg. 1), per row, branch-free.
-        // B0 blocks (and a first block with m = -inf) take the high-precision
-        // path; B1 blocks restart when ceil(rowmax T) > lambda, where rowmax of
-        // the 8-bit T = fl32(acc*c - m) is the 8-bit cast of the raw maximum's
-        // T (the cast is monotone).
-        const bool vis = amax != ninf;
-        const bool forced = (jb < p.n_b0) || (m == ninf);
-        const float tq = hif8::round(__builtin_fmaf(amax, c, -m));
-        const bool restart = forced || (ceilf(tq) > lam);
-        const float m_hi = __builtin_fmaxf(m, ceilf(amax * c));    // ceil(rowmax S), S in fp32
-        const float m_new = vis ? (restart ? m_hi : m + __builtin_fmaxf(0.0f, ceilf(tq))) : m;
-        const float ref_new = vis ? (restart ? m_hi : m) : ref;
-        const bool b1 = vis && (jb >= p.n_b0);
-        n_visit += b1 ? 1u : 0u;
-        n_restart += (b1 && restart) ? 1u : 0u;
-        const float f = (ref == ninf) ? 1.0f : exp2_int(ref - ref_new);
-        if (__any(f != 1.0f)) {
-#pragma unroll
-            for (int t = 0; t < kDT; ++t)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) oacc[t][i] *= f;
-        }
-        dl *= f;
-        m = m_new;
-        ref = ref_new;
+        float nref;
+        if constexpr (MODE == kModeE2E) {
+            // block-aware precision rescaling (Alg. 1), per row, branch-free.
+            // B0 blocks (and a first block with m = -inf) take the high-precision
+            // path; B1 blocks restart when ceil(rowmax T) > lambda, where rowmax of
+            // the 8-bit T = fl32(acc*c - m) is the 8-bit cast of the raw maximum's
+            // T (the cast is monotone).
+            const bool vis = amax != ninf;
+            const bool forced = (jb < p.n_b0) || (m == ninf);
+            const float tq = hif8::round(__builtin_fmaf(amax, c, -m));
+            const bool restart = forced || (ceilf(tq) > lam);
+            const float m_hi = __builtin_fmaxf(m, ceilf(amax * c));    // ceil(rowmax S), S in fp32
+            const float m_new = vis ? (restart ? m_hi : m + __builtin_fmaxf(0.0f, ceilf(tq))) : m;
+            const float ref_new = vis ? (restart ? m_hi : m) : ref;
+            const bool b1 = vis && (jb >= p.n_b0);
+            n_visit += b1 ? 1u : 0u;
+            n_restart += (b1 && restart) ? 1u : 0u;
+            const float f = (ref == ninf) ? 1.0f : exp2_int(ref - ref_new);
+            if (__any(f != 1.0f)) {
+    #pragma unroll
+                for (int t = 0; t < kDT; ++t)
+    #pragma unroll
+                    for (int i = 0; i < 16; ++i) oacc[t][i] *= f;
+            }
+            dl *= f;
+            m = m_new;
+            ref = ref_new;
 
-        // a row with no visible key so far keeps ref = -inf; its masked scores
-        // (acc = -inf) must still give T = -inf and P = 0
-        const float nref = (ref == ninf) ? 0.0f : -ref;
+            // a row with no visible key so far keeps ref = -inf; its masked scores
+            // (acc = -inf) must still give T = -inf and P = 0
+            nref = (ref == ninf) ? 0.0f : -ref;
+        } else {
+            // eq. (2): real-valued running maximum m, rescale factor
+            // 2^(m_old - m) in fp32 (Default) or HiF8(2^HiF8(m_old - m)) (Exp2 HiF8)
+            const bool vis = amax != ninf;
+            const float m_new = vis ? __builtin_fmaxf(m, amax * c) : m;   // fl32(max acc * c) = max S
+            float f = 1.0f;
+            if (m != ninf) {
+                const float x = m - m_new;
+                if constexpr (MODE == kModeDefault) {
+                    f = __builtin_amdgcn_exp2f(x);
+                } else {
+                    const uint32_t ix = min(max(hif8::f2u(x) >> kTabShift, (uint32_t)kCodeLo), (uint32_t)kCodeHi);
+                    f = hif8::u2f((uint32_t)ctab[ix] << 20) * 0x1p104f;
+                }
+            }
+            if (__any(f != 1.0f)) {
+#pragma unroll
+                for (int t = 0; t < kDT; ++t)
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) oacc[t][i] *= f;
+            }
+            dl *= f;
+            m = m_new;
+            ref = m_new;
+            nref = (m == ninf) ? 0.0f : -m;
+        }
+
         const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 #pragma unroll
         for (int kt = 0; kt < kKT; ++kt) {
@@ -351,9 +383,23 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
             for (int ch = 0; ch < 2; ++ch) {
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    const float t0 = __builtin_fmaf(sacc[kt][ch * 8 + 2 * e], c, nref);
-                    const float t1 = __builtin_fmaf(sacc[kt][ch * 8 + 2 * e + 1], c, nref);
                     uint32_t w;
+                    if constexpr (MODE == kModeDefault) {
+                        // P = 2^fl32(S - m) in fp32; bf16 into P V, fp32 into the sum
+                        const float p0 = __builtin_amdgcn_exp2f(sacc[kt][ch * 8 + 2 * e] * c + nref);
+                        const float p1 = __builtin_amdgcn_exp2f(sacc[kt][ch * 8 + 2 * e + 1] * c + nref);
+                        const bf16x2 pb = {(__bf16)p0, (__bf16)p1};
+                        w = __builtin_bit_cast(uint32_t, pb);
+                        dl += p0 + p1;
+                        pop[ch][e] = w;
+                        continue;
+                    }
+                    // T = fl32(acc*c - ref) rounded once (Alg. 1), or fl32(S - m) with
+                    // S = fl32(acc*c) (eq. (2), Exp2 HiF8)
+                    const float t0 = MODE == kModeE2E ? __builtin_fmaf(sacc[kt][ch * 8 + 2 * e], c, nref)
+                                                      : sacc[kt][ch * 8 + 2 * e] * c + nref;
+                    const float t1 = MODE == kModeE2E ? __builtin_fmaf(sacc[kt][ch * 8 + 2 * e + 1], c, nref)
+                                                      : sacc[kt][ch * 8 + 2 * e + 1] * c + nref;
                     if constexpr (CT) {
                         // two bf16 of P * 2^-kCodeBiasLog2
                         const uint32_t i0 = min(max(hif8::f2u(t0) >> kTabShift, (uint32_t)kCodeLo), (uint32_t)kCodeHi);
@@ -386,7 +432,7 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
     // epilogue: O = X / dX, lse = ln2 (ref + log2 dX) = ln2 (m + log2 d);
     // with the compact table X and dX carry the factor 2^-kCodeBiasLog2
     const float d = dl + __shfl_xor(dl, 32, 64);
-    const float dbias = CT ? (float)kCodeBiasLog2 : 0.0f;
+    const float dbias = (CT && MODE != kModeDefault) ? (float)kCodeBiasLog2 : 0.0f;
     if (!row_ok) return;
     float* orow = p.o + (((long long)b * p.Hq + h) * p.Sq + r) * D;
     const bool empty = (ref == ninf);
@@ -409,20 +455,20 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
     }
 }
 
-template <int D, int BLK, int NW, bool CT>
+template <int D, int BLK, int NW, bool CT, int MODE>
 hipError_t launch_one(const AttnParams& p, hipStream_t st)
 {
     using C = Cfg<D, BLK, NW>;
     static bool attr_set = false;
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&baps_attn_fwd_kernel<D, BLK, NW, CT>),
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&baps_attn_fwd_kernel<D, BLK, NW, CT, MODE>),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, C::kLdsBytes);
         if (e != hipSuccess) return e;
         attr_set = true;
     }
     const long long flat = (long long)p.Sq * (p.Hq / p.Hkv);
     const dim3 grid((unsigned)((flat + C::kTileRows - 1) / C::kTileRows), (unsigned)p.Hkv, (unsigned)p.B);
-    hipLaunchKernelGGL((baps_attn_fwd_kernel<D, BLK, NW, CT>), grid, dim3(C::kThreads), C::kLdsBytes, st, p);
+    hipLaunchKernelGGL((baps_attn_fwd_kernel<D, BLK, NW, CT, MODE>), grid, dim3(C::kThreads), C::kLdsBytes, st, p);
     return hipGetLastError();
 }
 
@@ -432,8 +478,10 @@ hipError_t launch_d_blk(const AttnParams& p, hipStream_t st)
     // few rows per key/value head (decode, short queries): the HBM-streaming kernel
     const long long flat = (long long)p.Sq * (p.Hq / p.Hkv);
     if (flat <= 64) return launch_attention_decode(p, D, BLK, st);
-    if (p.lambda <= kCodeMaxLambda) return launch_one<D, BLK, 8, true>(p, st);
-    return launch_one<D, BLK, 8, false>(p, st);
+    if (p.mode == kModeDefault) return launch_one<D, BLK, 8, true, kModeDefault>(p, st);
+    if (p.mode == kModeExp2) return launch_one<D, BLK, 8, true, kModeExp2>(p, st);
+    if (p.lambda <= kCodeMaxLambda) return launch_one<D, BLK, 8, true, kModeE2E>(p, st);
+    return launch_one<D, BLK, 8, false, kModeE2E>(p, st);
 }
 
 }  // namespace

@@ -37,6 +37,14 @@ constexpr int kCodeEntries = kCodeHi - kCodeLo + 1;
 constexpr int kCodeBiasLog2 = 104;
 constexpr int kCodeMaxLambda = 8;
 
+// Softmax setups of the fused attention kernels: the proposed workflow
+// (Alg. 1, "E2E HiF8") and two setups of eq. (2) with a real-valued running
+// maximum, "Default" (fp32 exp2) and "Exp2 HiF8" (the exp2 evaluated on 8-bit
+// input and rounded to 8 bits), for comparison on the same tiling.
+constexpr int kModeE2E = 0;
+constexpr int kModeDefault = 1;
+constexpr int kModeExp2 = 2;
+
 struct AttnParams {
     const uint16_t* q;          // [B, Hq, Sq, D] bf16
     const uint16_t* k;          // [B, Hkv, Sk, D] bf16
@@ -48,6 +56,7 @@ struct AttnParams {
     unsigned long long* counters;  // [B*Hq][2] restarted / visited B1 row-blocks, or null
     int B, Hq, Hkv, Sq, Sk;
     int causal, lambda, n_b0;
+    int mode;                   // kModeE2E, kModeDefault or kModeExp2
     float c;                    // log2(e)/sqrt(D) as fp32 (or the caller's override)
 };
 

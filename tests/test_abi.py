@@ -63,8 +63,16 @@ def test_attention_argument_checks(lib):
     assert _attn(lib, block=48) == 2
     assert _attn(lib, B=0) == 0                  # empty work
     assert _attn(lib, Sq=0, q=None, o=None) == 0
-    prm = baps.baps_params_t(1, 1, -1.0, None)
+    prm = baps.baps_params_t(1, 1, -1.0, None, 0)
     assert lib.baps_attention_fwd_ex(16, 16, 16, 16, None, 1, 1, 1, 4, 4, 64, 0, 64, ctypes.byref(prm), None) == 1
+    for bad_mode in (-1, 3, 7):                  # softmax setup out of range
+        prm = baps.baps_params_t(1, 1, 0.0, None, bad_mode)
+        assert lib.baps_attention_fwd_ex(16, 16, 16, 16, None, 1, 1, 1, 4, 4, 64, 0, 64, ctypes.byref(prm),
+                                         None) == 1
+    for mode in (baps.BAPS_MODE_DEFAULT, baps.BAPS_MODE_EXP2_HIF8):   # valid, empty work
+        prm = baps.baps_params_t(1, 1, 0.0, None, mode)
+        assert lib.baps_attention_fwd_ex(16, 16, 16, 16, None, 0, 1, 1, 4, 4, 64, 0, 64, ctypes.byref(prm),
+                                         None) == 0
     assert lib.baps_attention_fwd_ex(16, 16, 16, 16, None, 1, 1, 1, 4, 4, 64, 0, 64, None, None) == 1
 
 

@@ -264,3 +264,52 @@ def test_margin_marks_rows_stable_under_valid_scores():
         assert diff[det].max() <= 1e-3
         moved_amb += int((diff[~det] > 0).sum())
     assert moved_amb > 0
+
+
+def test_exp2_hif8_margin_marks_rows_stable_under_valid_scores():
+    # Exp2 HiF8 (eq. 2 with the exp2 in 8 bits): rows whose HiF8 roundings
+    # all clear their boundaries by the accumulation error bound give the
+    # same 8-bit P and alpha, hence the same O, for every valid high-precision S
+    args = _args(1, 4, 2, 160, 300, 128, True, seed=17, outliers=True)
+    o, _, _, mg = O.attention(*args, 64, mode=O.EXP2_HIF8, margin=True)
+    det = mg >= 1
+    assert det.sum() > 0.5 * det.size
+    moved_amb = 0
+    for scale, seed in ((1.0, 0), (-1.0, 0), (0.7, 3), (1.0, 9)):
+        oj, _, _ = O.attention(*args, 64, mode=O.EXP2_HIF8, jitter=scale, jitter_seed=seed)
+        diff = np.abs(oj - o).max(axis=1)
+        assert diff[det].max() <= 1e-5
+        moved_amb += int((diff[~det] > 1e-5).sum())
+    assert moved_amb > 0
+    # the Default setup has no 8-bit decision: every row is determined,
+    # unless P is rounded to bf16 for the P V product, whose roundings are
+    # decisions as well (and the same rule holds for them)
+    _, _, _, mgd = O.attention(*args, 64, mode=O.DEFAULT, margin=True)
+    assert np.all(np.isinf(mgd))
+    od, _, _, mgb = O.attention(*args, 64, mode=O.DEFAULT, margin=True, pv_bf16=True)
+    detb = mgb >= 1
+    assert 0.3 * detb.size < detb.sum() < detb.size
+    for scale, seed in ((1.0, 0), (-1.0, 0), (1.0, 9)):
+        oj, _, _ = O.attention(*args, 64, mode=O.DEFAULT, pv_bf16=True, jitter=scale, jitter_seed=seed)
+        # a moved score moves P continuously (here up to ~3e-4 relative: the
+        # outlier channels make the accumulation bound large); a bf16 flip of
+        # a dominant P would move O by ~2^-8 |v|, which determined rows must not
+        assert np.abs(oj - od).max(axis=1)[detb].max() <= 1.5e-3
+
+
+def test_pv_bf16_rounding_bound():
+    # pv_bf16 rounds each P to bf16 (relative error <= 2^-9) only inside the
+    # P V product: O moves by at most 2^-9 * sum_c p_c |v_c| / d, and not at
+    # all when every P is a power of two (integer scores)
+    q, k, v, *shape = _args(1, 2, 1, 40, 90, 32, True, seed=23)
+    B, Hq, Hkv, Sq, Sk, D, causal = shape
+    o32, _, _ = O.attention(q, k, v, *shape, 32, mode=O.DEFAULT)
+    o16, _, _ = O.attention(q, k, v, *shape, 32, mode=O.DEFAULT, pv_bf16=True)
+    vmax = np.abs(bf16_bits_to_f32(v)).max()
+    assert 0 < np.abs(o16 - o32).max() <= 2.0 ** -9 * vmax * 1.01
+    g = np.random.default_rng(3)
+    qi = f32_to_bf16_bits(g.integers(-1, 2, (1, 2, 40, 32)).astype(np.float32))
+    ki = f32_to_bf16_bits(g.integers(-1, 2, (1, 1, 90, 32)).astype(np.float32))
+    a32, _, _ = O.attention(qi, ki, v, *shape, 32, mode=O.DEFAULT, scale_log2=1.0)
+    a16, _, _ = O.attention(qi, ki, v, *shape, 32, mode=O.DEFAULT, scale_log2=1.0, pv_bf16=True)
+    assert np.array_equal(a32, a16)
