@@ -134,6 +134,34 @@ def softmax_setups(cfg, steps=20):
     return res
 
 
+def single_sequence_decode(steps=20):
+    """One sequence, long context (B=1, Hq=32, Hkv=8, Sq=1, Sk=32768, D=128,
+    block 128): the one-pass decode kernel (8 streams) against the split-key
+    path.  HBM GB/s of Q, K, V, O and lse per call."""
+    import torch
+    import paper_2602_02071_amd as baps
+    from paper_2602_02071_amd.workloads import Workload, make_qkv
+    w = Workload("single decode sk32768 gqa32/8 d128", 1, 32, 8, 1, 32768, 128, False, 128, lognormal_k=True)
+    q, k, v = make_qkv(w.B, w.Hq, w.Hkv, w.Sq, w.Sk, w.D, seed=6, lognormal_k=True)
+    dev = torch.device("cuda:0")
+    qt, kt, vt = (torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).to(dev) for x in (q, k, v))
+    o = torch.empty((w.B, w.Hq, w.Sq, w.D), dtype=torch.float32, device=dev)
+    lse = torch.empty((w.B, w.Hq, w.Sq), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream().cuda_stream
+    nbytes = baps.baps_attention_split_workspace(w.B, w.Hq, w.Hkv, w.Sq, w.Sk, w.D, w.block)
+    ws = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+    res = {"workload": w.name, "workspace_bytes": nbytes}
+    for name, fn in (("one_pass", lambda: baps.baps_attention_fwd(qt, kt, vt, o, lse, w.B, w.Hq, w.Hkv, w.Sq, w.Sk,
+                                                                   w.D, w.causal, w.block, stream)),
+                     ("split", lambda: baps.baps_attention_fwd_split(qt, kt, vt, o, lse, w.B, w.Hq, w.Hkv, w.Sq, w.Sk,
+                                                                      w.D, w.causal, w.block, ws, nbytes,
+                                                                      stream=stream))):
+        wall, per = _time_launches(fn, steps, 3, 50.0)
+        ms = wall * 1e3 / steps
+        res[name] = {"us": ms * 1e3, "GB/s": w.bytes_qkvo / (ms * 1e-3) / 1e9}
+    return res
+
+
 def boundary_kernels(steps=10):
     """Throughput of the standalone boundary kernels on HBM-sized inputs:
     hif8_encode / hif8_decode over 2^28 elements (1 GiB of fp32, beyond the
@@ -254,6 +282,8 @@ def main():
                                       "frac": gbs / PEAK_HBM_GBS, "traffic": _traffic("attn_fwd_decode")}}
     if not args.no_modes and w.Sq > 1:
         out["softmax_setups"] = softmax_setups(args.config)
+    if not args.no_decode and args.config != 3:
+        out["decode_single_sequence"] = single_sequence_decode()
     if not args.no_boundary:
         out["boundary"] = boundary_kernels()
     if not args.no_cpu_baseline:

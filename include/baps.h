@@ -93,6 +93,37 @@ int baps_attention_fwd_ex(const void* q, const void* k, const void* v, float* o,
                           const baps_params_t* p, void* stream);
 
 /*
+ * Split-key path for few query rows per key/value head (single-sequence or
+ * small-batch decode over long contexts: few (batch, key/value head) streams,
+ * many keys).  Alg. 1's state after a key block depends on the keys only
+ * through the block's row maximum, so the call runs as passes over key
+ * splits: raw dot products and block maxima of every split in parallel; then,
+ * per split in parallel, a per-row replay of the B0 / restart rule and
+ * integer maximum in block order up to the split's last block and P V of the
+ * split at those references; last, per row, an exact power-of-two combine.  Every T, P and reference equals baps_attention_fwd_ex's;
+ * O and lse differ only by the order of fp32 additions.
+ *
+ * baps_attention_split_workspace: the workspace bytes the call needs for this
+ * shape and these knobs (p may be NULL: canonical knobs); 0 when the shape
+ * takes the one-pass kernels (more than 64 flattened rows per key/value head,
+ * enough streams to fill the GPU, fewer than 4 key blocks, a setup other
+ * than BAPS_MODE_E2E_HIF8, or lambda > 8).
+ *
+ * baps_attention_fwd_split: baps_attention_fwd_ex (p may be NULL: canonical
+ * knobs) with a caller-owned device workspace of at least that many bytes,
+ * 256-byte aligned, contents undefined on entry and on return; NULL and 0 are
+ * fine when the size is 0.  Status 1 when a needed workspace is missing,
+ * short or misaligned.  Asynchronous on the stream; the workspace must not be
+ * reused before the call completes.
+ */
+long long baps_attention_split_workspace(int B, int Hq, int Hkv, int Sq, int Sk, int D, int block,
+                                         const baps_params_t* p);
+int baps_attention_fwd_split(const void* q, const void* k, const void* v, float* o, float* lse,
+                             int B, int Hq, int Hkv, int Sq, int Sk, int D, int causal, int block,
+                             const baps_params_t* p, void* workspace, long long workspace_bytes,
+                             void* stream);
+
+/*
  * HiF8 codec (the 8-bit format used by every 8-bit step of the method;
  * Sec. 2, App. A).  hif8_encode: codes[i] = code of the HiF8 value nearest
  * to x[i] (ties away from zero).  flags: BAPS_HIF8_SATURATE clamps finite
@@ -135,6 +166,11 @@ int baps_get_exp2_lut(unsigned char out_codes[256]);
 /* Uploads the score table to the current device (synchronously).  Optional:
  * the first call of an entry point on a device does it otherwise. */
 int baps_init(void);
+
+/* Name of the last HIP runtime error that a call of this library met on the
+ * calling thread ("hipSuccess" if none): the detail behind BAPS_HIP_ERROR.
+ * Static storage; not cleared by later successful calls. */
+const char* baps_last_hip_error(void);
 
 /* Text of a status code (static storage). */
 const char* baps_status_string(int status);

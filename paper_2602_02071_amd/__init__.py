@@ -19,15 +19,17 @@ BAPS_UNSUPPORTED = 2
 BAPS_HIP_ERROR = 3
 BAPS_HIF8_SATURATE = 1
 
-EXPORTS = ("baps_attention_fwd", "baps_attention_fwd_ex", "hif8_encode", "hif8_decode",
-           "baps_softmax_block", "baps_get_exp2_lut", "baps_init", "baps_status_string")
+EXPORTS = ("baps_attention_fwd", "baps_attention_fwd_ex", "baps_attention_fwd_split", "hif8_encode",
+           "hif8_decode", "baps_softmax_block", "baps_get_exp2_lut", "baps_init",
+           "baps_attention_split_workspace", "baps_last_hip_error", "baps_status_string")
 
 _lib = None
 
 
 class BapsError(RuntimeError):
     def __init__(self, fn, status):
-        super().__init__(f"{fn}: {status_string(status)} (status {status})")
+        detail = f", {load().baps_last_hip_error().decode()}" if status == 3 else ""
+        super().__init__(f"{fn}: {status_string(status)} (status {status}{detail})")
         self.status = status
 
 
@@ -49,11 +51,19 @@ def load():
         return _lib
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is missing: run __graft_entry__.build() (hipcc, gfx950) first")
+    # torch ships its own HIP and HSA runtimes under the same sonames as the
+    # system ones; with torch loaded first the library binds to them, so the
+    # process holds one runtime (two would both claim the GPU, and the second
+    # to start up finds no device).
+    import torch  # noqa: F401
     L = ctypes.CDLL(LIB_PATH)
     P, I, LL = ctypes.c_void_p, ctypes.c_int, ctypes.c_longlong
     L.baps_attention_fwd.argtypes = [P, P, P, P, P, I, I, I, I, I, I, I, I, P]
     L.baps_attention_fwd_ex.argtypes = [P, P, P, P, P, I, I, I, I, I, I, I, I,
                                         ctypes.POINTER(baps_params_t), P]
+    L.baps_attention_fwd_split.argtypes = [P, P, P, P, P, I, I, I, I, I, I, I, I,
+                                           ctypes.POINTER(baps_params_t), P, LL, P]
+    L.baps_attention_split_workspace.argtypes = [I, I, I, I, I, I, I, ctypes.POINTER(baps_params_t)]
     L.hif8_encode.argtypes = [P, P, LL, I, P]
     L.hif8_decode.argtypes = [P, P, LL, P]
     L.baps_softmax_block.argtypes = [P, LL, LL, LL, I, I, I, I, P, P, P, P, P, P]
@@ -61,8 +71,11 @@ def load():
     L.baps_init.argtypes = []
     L.baps_status_string.argtypes = [I]
     L.baps_status_string.restype = ctypes.c_char_p
-    for name in EXPORTS[:-1]:
+    L.baps_last_hip_error.argtypes = []
+    L.baps_last_hip_error.restype = ctypes.c_char_p
+    for name in EXPORTS[:-2]:
         getattr(L, name).restype = I
+    L.baps_attention_split_workspace.restype = LL
     _lib = L
     return L
 
@@ -107,6 +120,21 @@ def baps_attention_fwd_ex(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block,
         ctypes.byref(prm), _stream(stream)))
 
 
+def baps_attention_split_workspace(B, Hq, Hkv, Sq, Sk, D, block, lam=1, n_b0=1, scale_log2=0.0,
+                                   mode=BAPS_MODE_E2E_HIF8):
+    prm = baps_params_t(int(lam), int(n_b0), float(scale_log2), None, int(mode))
+    return int(load().baps_attention_split_workspace(B, Hq, Hkv, Sq, Sk, D, block, ctypes.byref(prm)))
+
+
+def baps_attention_fwd_split(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, workspace, workspace_bytes,
+                             lam=1, n_b0=1, scale_log2=0.0, restart_counts=None, stream=None,
+                             mode=BAPS_MODE_E2E_HIF8):
+    prm = baps_params_t(int(lam), int(n_b0), float(scale_log2), _p(restart_counts), int(mode))
+    _check("baps_attention_fwd_split", load().baps_attention_fwd_split(
+        _p(q), _p(k), _p(v), _p(o), _p(lse), B, Hq, Hkv, Sq, Sk, D, int(causal), block,
+        ctypes.byref(prm), _p(workspace), int(workspace_bytes), _stream(stream)))
+
+
 def hif8_encode(x, codes, n, flags=BAPS_HIF8_SATURATE, stream=None):
     _check("hif8_encode", load().hif8_encode(_p(x), _p(codes), n, flags, _stream(stream)))
 
@@ -134,9 +162,10 @@ def baps_init():
 
 # ------------------------------------------------------------ tensor helpers
 def attention(q, k, v, causal, block, lse=True, lam=None, n_b0=None, scale_log2=0.0, restart_counts=None,
-              stream=None, mode=BAPS_MODE_E2E_HIF8):
+              stream=None, mode=BAPS_MODE_E2E_HIF8, split=False):
     """Allocate O (and lse) with torch on q's device and run the fused pass.
-    q [B,Hq,Sq,D], k/v [B,Hkv,Sk,D] bf16 CUDA tensors, contiguous."""
+    q [B,Hq,Sq,D], k/v [B,Hkv,Sk,D] bf16 CUDA tensors, contiguous.  split:
+    take baps_attention_fwd_split, with a workspace allocated here."""
     import torch
     B, Hq, Sq, D = q.shape
     Hkv, Sk = k.shape[1], k.shape[2]
@@ -145,7 +174,13 @@ def attention(q, k, v, causal, block, lse=True, lam=None, n_b0=None, scale_log2=
             raise ValueError("q, k, v must be contiguous bf16 device tensors")
     o = torch.empty((B, Hq, Sq, D), dtype=torch.float32, device=q.device)
     l = torch.empty((B, Hq, Sq), dtype=torch.float32, device=q.device) if lse else None
-    if lam is None and n_b0 is None and not scale_log2 and restart_counts is None and mode == BAPS_MODE_E2E_HIF8:
+    if split:
+        lam_, nb_ = 1 if lam is None else lam, 1 if n_b0 is None else n_b0
+        nbytes = baps_attention_split_workspace(B, Hq, Hkv, Sq, Sk, D, block, lam_, nb_, scale_log2, mode)
+        ws = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=q.device)
+        baps_attention_fwd_split(q, k, v, o, l, B, Hq, Hkv, Sq, Sk, D, causal, block, ws, nbytes, lam_, nb_,
+                                 scale_log2, restart_counts, stream, mode)
+    elif lam is None and n_b0 is None and not scale_log2 and restart_counts is None and mode == BAPS_MODE_E2E_HIF8:
         baps_attention_fwd(q, k, v, o, l, B, Hq, Hkv, Sq, Sk, D, causal, block, stream)
     else:
         baps_attention_fwd_ex(q, k, v, o, l, B, Hq, Hkv, Sq, Sk, D, causal, block,

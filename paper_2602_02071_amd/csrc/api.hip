@@ -82,22 +82,40 @@ std::mutex g_mutex;
 const uint32_t* g_dev_table[kMaxDevices] = {};
 const uint8_t* g_dev_code[kMaxDevices] = {};
 
+// the last HIP failure a call of this library met on the calling thread
+thread_local hipError_t g_last_hip = hipSuccess;
+
+int status_of(hipError_t e)
+{
+    if (e == hipSuccess) return BAPS_OK;
+    g_last_hip = e;
+    return BAPS_HIP_ERROR;
+}
+
+// HIP keeps the last failed call's error until it is read, whoever made the
+// call (the runtime's own start-up included); the launchers read it after
+// their launches, so it is cleared first: a launch is judged on its own.
+void clear_stale_error() { (void)hipGetLastError(); }
+
 int table_on_current_device(const uint32_t** out, const uint8_t** code = nullptr)
 {
     int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess) return BAPS_HIP_ERROR;
+    if (int st = status_of(hipGetDevice(&dev))) return st;
     if (dev < 0 || dev >= kMaxDevices) return BAPS_UNSUPPORTED;
     std::lock_guard<std::mutex> lock(g_mutex);
     if (!g_dev_table[dev]) {
         const Table& t = host_table();
-        if (hipMemcpyToSymbol(HIP_SYMBOL(g_score_table), t.e, sizeof(t.e), 0, hipMemcpyHostToDevice) != hipSuccess)
-            return BAPS_HIP_ERROR;
+        if (int st = status_of(hipMemcpyToSymbol(HIP_SYMBOL(g_score_table), t.e, sizeof(t.e), 0,
+                                                 hipMemcpyHostToDevice)))
+            return st;
         void* ptr = nullptr;
-        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(g_score_table)) != hipSuccess || !ptr) return BAPS_HIP_ERROR;
-        if (hipMemcpyToSymbol(HIP_SYMBOL(g_code_table), t.code, sizeof(t.code), 0, hipMemcpyHostToDevice) != hipSuccess)
-            return BAPS_HIP_ERROR;
+        if (int st = status_of(hipGetSymbolAddress(&ptr, HIP_SYMBOL(g_score_table)))) return st;
+        if (int st = status_of(hipMemcpyToSymbol(HIP_SYMBOL(g_code_table), t.code, sizeof(t.code), 0,
+                                                 hipMemcpyHostToDevice)))
+            return st;
         void* cptr = nullptr;
-        if (hipGetSymbolAddress(&cptr, HIP_SYMBOL(g_code_table)) != hipSuccess || !cptr) return BAPS_HIP_ERROR;
+        if (int st = status_of(hipGetSymbolAddress(&cptr, HIP_SYMBOL(g_code_table)))) return st;
+        if (!ptr || !cptr) return BAPS_HIP_ERROR;
         g_dev_code[dev] = static_cast<const uint8_t*>(cptr);
         g_dev_table[dev] = static_cast<const uint32_t*>(ptr);
     }
@@ -108,7 +126,6 @@ int table_on_current_device(const uint32_t** out, const uint8_t** code = nullptr
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
-int status_of(hipError_t e) { return e == hipSuccess ? BAPS_OK : BAPS_HIP_ERROR; }
 
 int attention_impl(const void* q, const void* k, const void* v, float* o, float* lse, int B, int Hq,
                    int Hkv, int Sq, int Sk, int D, int causal, int block, int lambda, int n_b0,
@@ -144,12 +161,118 @@ int attention_impl(const void* q, const void* k, const void* v, float* o, float*
     p.n_b0 = n_b0;
     p.mode = mode;
     p.c = scale_log2 > 0.0f ? scale_log2 : (float)(1.4426950408889634 / std::sqrt((double)D));
+    clear_stale_error();
     return status_of(launch_attention(p, D, block, static_cast<hipStream_t>(stream)));
+}
+
+// The split-key plan of a call: used for few rows per key/value head (the
+// decode kernels' regime), few (batch, key/value head) row tiles and many
+// key blocks, in the E2E HiF8 setup with the compact code table.
+struct SplitPlan {
+    bool use = false;
+    int nblk = 0, bstride = 0, nsplit = 0, bps = 0;
+    long long off_acc = 0, off_bmax = 0, off_part = 0, bytes = 0;
+};
+
+long long align256(long long x) { return (x + 255) & ~255LL; }
+
+SplitPlan split_plan(int B, int Hq, int Hkv, int Sq, int Sk, int D, int block, int lambda, int mode)
+{
+    SplitPlan sp;
+    if (B <= 0 || Hq <= 0 || Hkv <= 0 || Sq <= 0 || Sk <= 0 || Hq % Hkv) return sp;
+    if (!(D == 64 || D == 128) || !(block == 32 || block == 64 || block == 128)) return sp;
+    if (mode != BAPS_MODE_E2E_HIF8 || lambda > kCodeMaxLambda) return sp;
+    const long long flat = (long long)Sq * (Hq / Hkv);
+    if (flat > 64) return sp;                                   // the prefill kernel's regime
+    const long long tiles = (flat + 15) / 16;
+    const long long streams = (long long)B * Hkv * tiles;
+    const int nblk = (Sk + block - 1) / block;
+    if (streams >= 256 || nblk < 4) return sp;                  // already enough workgroups
+    long long want = (512 + streams - 1) / streams;             // about two workgroups per CU
+    const long long fewest = (nblk + kSplitMaxBps - 1) / kSplitMaxBps;
+    if (want < fewest) want = fewest;
+    const int ns0 = (int)(want < nblk ? want : nblk);
+    sp.bps = (nblk + ns0 - 1) / ns0;
+    sp.nsplit = (nblk + sp.bps - 1) / sp.bps;
+    if (sp.nsplit < 2) return sp;
+    sp.use = true;
+    sp.nblk = nblk;
+    sp.bstride = (nblk + 63) / 64 * 64;
+    const long long rows = (long long)B * Hkv * flat;
+    long long off = 0;
+    sp.off_acc = off;    off += align256(rows * nblk * (long long)block * 4);
+    sp.off_bmax = off;   off += align256(rows * sp.bstride * 4);
+    sp.off_part = off;   off += align256((long long)sp.nsplit * rows * (D + 4) * 4);
+    sp.bytes = off;
+    return sp;
 }
 
 }  // namespace
 
 extern "C" {
+
+long long baps_attention_split_workspace(int B, int Hq, int Hkv, int Sq, int Sk, int D, int block,
+                                         const baps_params_t* prm)
+{
+    const int lambda = prm ? prm->lambda : 1;
+    const int mode = prm ? prm->mode : BAPS_MODE_E2E_HIF8;
+    const SplitPlan sp = split_plan(B, Hq, Hkv, Sq, Sk, D, block, lambda, mode);
+    return sp.use ? sp.bytes : 0;
+}
+
+int baps_attention_fwd_split(const void* q, const void* k, const void* v, float* o, float* lse, int B, int Hq,
+                             int Hkv, int Sq, int Sk, int D, int causal, int block, const baps_params_t* prm,
+                             void* workspace, long long workspace_bytes, void* stream)
+{
+    try {
+        const int lambda = prm ? prm->lambda : 1;
+        const int n_b0 = prm ? prm->n_b0 : 1;
+        const float scale_log2 = prm ? prm->scale_log2 : 0.0f;
+        unsigned long long* counters = prm ? prm->restart_counts : nullptr;
+        const int mode = prm ? prm->mode : BAPS_MODE_E2E_HIF8;
+        const SplitPlan plan = split_plan(B, Hq, Hkv, Sq, Sk, D, block, lambda, mode);
+        if (!plan.use)
+            return attention_impl(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, lambda, n_b0,
+                                  scale_log2, counters, mode, stream);
+        // the same argument checks as the one-pass path (they pass or fail alike)
+        if (n_b0 < 0 || !(scale_log2 >= 0.0f) || std::isinf(scale_log2)) return BAPS_INVALID_ARGUMENT;
+        if (!q || !o || !k || !v) return BAPS_INVALID_ARGUMENT;
+        if (!aligned16(q) || !aligned16(o) || !aligned16(k) || !aligned16(v)) return BAPS_INVALID_ARGUMENT;
+        if (!workspace || workspace_bytes < plan.bytes || ((uintptr_t)workspace & 255u)) return BAPS_INVALID_ARGUMENT;
+        const uint32_t* tab = nullptr;
+        const uint8_t* ctab = nullptr;
+        int st = table_on_current_device(&tab, &ctab);
+        if (st) return st;
+        SplitParams sp;
+        AttnParams& p = sp.a;
+        p.q = static_cast<const uint16_t*>(q);
+        p.k = static_cast<const uint16_t*>(k);
+        p.v = static_cast<const uint16_t*>(v);
+        p.o = o;
+        p.lse = lse;
+        p.tab = tab;
+        p.ctab = ctab;
+        p.counters = counters;
+        p.B = B; p.Hq = Hq; p.Hkv = Hkv; p.Sq = Sq; p.Sk = Sk;
+        p.causal = causal ? 1 : 0;
+        p.lambda = lambda;
+        p.n_b0 = n_b0;
+        p.mode = mode;
+        p.c = scale_log2 > 0.0f ? scale_log2 : (float)(1.4426950408889634 / std::sqrt((double)D));
+        char* ws = static_cast<char*>(workspace);
+        sp.acc = reinterpret_cast<float*>(ws + plan.off_acc);
+        sp.bmax = reinterpret_cast<float*>(ws + plan.off_bmax);
+        sp.part = reinterpret_cast<float*>(ws + plan.off_part);
+        sp.nblk = plan.nblk;
+        sp.bstride = plan.bstride;
+        sp.nsplit = plan.nsplit;
+        sp.bps = plan.bps;
+        clear_stale_error();
+        return status_of(launch_attention_split(sp, D, block, static_cast<hipStream_t>(stream)));
+    } catch (...) {
+        return BAPS_HIP_ERROR;
+    }
+}
 
 int baps_attention_fwd(const void* q, const void* k, const void* v, float* o, float* lse, int B, int Hq,
                        int Hkv, int Sq, int Sk, int D, int causal, int block, void* stream)
@@ -180,6 +303,7 @@ int hif8_encode(const float* x, unsigned char* codes, long long n, int flags, vo
     if (n < 0 || (flags & ~BAPS_HIF8_SATURATE)) return BAPS_INVALID_ARGUMENT;
     if (n == 0) return BAPS_OK;
     if (!x || !codes) return BAPS_INVALID_ARGUMENT;
+    clear_stale_error();
     return status_of(launch_hif8_encode(x, codes, n, (flags & BAPS_HIF8_SATURATE) != 0,
                                         static_cast<hipStream_t>(stream)));
 }
@@ -189,6 +313,7 @@ int hif8_decode(const unsigned char* codes, float* x, long long n, void* stream)
     if (n < 0) return BAPS_INVALID_ARGUMENT;
     if (n == 0) return BAPS_OK;
     if (!x || !codes) return BAPS_INVALID_ARGUMENT;
+    clear_stale_error();
     return status_of(launch_hif8_decode(codes, x, n, static_cast<hipStream_t>(stream)));
 }
 
@@ -210,6 +335,7 @@ int baps_softmax_block(const float* s, long long rows, long long cols, long long
         p.block = block; p.lambda = lambda; p.n_b0 = n_b0;
         p.codes = p_codes; p.ref_shift = ref_shift; p.m_final = m_final; p.d_final = d_final;
         p.restarted = restarted; p.tab = tab;
+        clear_stale_error();
         return status_of(launch_softmax_block(p, static_cast<hipStream_t>(stream)));
     } catch (...) {
         return BAPS_HIP_ERROR;
@@ -231,6 +357,11 @@ int baps_init(void)
     } catch (...) {
         return BAPS_HIP_ERROR;
     }
+}
+
+const char* baps_last_hip_error(void)
+{
+    return hipGetErrorName(g_last_hip);
 }
 
 const char* baps_status_string(int status)

@@ -72,6 +72,25 @@ struct SoftmaxBlockParams {
     const uint32_t* tab;
 };
 
+// The split-key path of the few-rows kernels (decode with few (batch, KV
+// head) streams and many keys).  Alg. 1's state after block j depends on the
+// key blocks only through their row maxima, so the path runs in passes over
+// a caller-provided workspace: the raw dot products and block maxima of every
+// key split in parallel; then, per split in parallel, a per-row scan of Alg.
+// 1's restart rule and integer maximum up to the split and P V at the
+// references of that scan; last, per row, an exact power-of-two combine.
+// The result is the sequential one up to the order of fp32 additions.
+struct SplitParams {
+    AttnParams a;               // the attention call (mode kModeE2E, lambda <= kCodeMaxLambda)
+    float* acc;                 // [B*Hkv][flat][nblk*BLK] raw dot products q.k (-inf when masked)
+    float* bmax;                // [B*Hkv][flat][bstride] raw row maximum of every key block
+    float* part;                // [nsplit][B*Hkv][flat][D + 4] X, dX and the reference they are relative to
+    int nblk, bstride;          // key blocks, and the block-maximum row stride (a multiple of 64)
+    int nsplit, bps;            // splits, blocks per split (at most kSplitMaxBps)
+};
+
+constexpr int kSplitMaxBps = 32;  // key blocks per split of the split-key path
+
 // exact 2^k for an integer-valued float k (0 below the fp32 range)
 __device__ __forceinline__ float exp2_int(float k)
 {
@@ -125,5 +144,6 @@ hipError_t launch_hif8_decode(const uint8_t* codes, float* x, long long n, hipSt
 hipError_t launch_softmax_block(const SoftmaxBlockParams& p, hipStream_t st);
 hipError_t launch_attention(const AttnParams& p, int D, int block, hipStream_t st);
 hipError_t launch_attention_decode(const AttnParams& p, int D, int block, hipStream_t st);
+hipError_t launch_attention_split(const SplitParams& sp, int D, int block, hipStream_t st);
 
 }  // namespace baps

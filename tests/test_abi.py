@@ -16,7 +16,8 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 def _declared():
     src = open(os.path.join(ROOT, "include", "baps.h")).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(\w+)\s*\(", src, flags=re.M)))
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?(?:(?:unsigned|long|short)\s+)*\w+[\s*]+(\w+)\s*\(",
+                                 src, flags=re.M)))
 
 
 @pytest.fixture(scope="module")
@@ -74,6 +75,25 @@ def test_attention_argument_checks(lib):
         assert lib.baps_attention_fwd_ex(16, 16, 16, 16, None, 0, 1, 1, 4, 4, 64, 0, 64, ctypes.byref(prm),
                                          None) == 0
     assert lib.baps_attention_fwd_ex(16, 16, 16, 16, None, 1, 1, 1, 4, 4, 64, 0, 64, None, None) == 1
+
+
+def test_split_workspace_and_checks(lib):
+    P = ctypes.POINTER(baps.baps_params_t)
+    # the split path is taken for few streams and many keys only
+    assert baps.baps_attention_split_workspace(1, 32, 8, 1, 32768, 128, 128) > 0
+    assert baps.baps_attention_split_workspace(64, 32, 8, 1, 8192, 128, 128) == 0      # enough streams
+    assert baps.baps_attention_split_workspace(1, 32, 8, 4096, 4096, 128, 128) == 0    # prefill regime
+    assert baps.baps_attention_split_workspace(1, 32, 8, 1, 256, 128, 128) == 0        # 2 key blocks
+    assert baps.baps_attention_split_workspace(1, 32, 8, 1, 32768, 128, 128, lam=9) == 0
+    assert baps.baps_attention_split_workspace(1, 32, 8, 1, 32768, 128, 128, mode=1) == 0
+    need = baps.baps_attention_split_workspace(1, 32, 8, 1, 32768, 128, 128)
+    # a needed workspace that is missing, short or misaligned is an invalid argument (no GPU work)
+    args = (16, 16, 16, 16, None, 1, 32, 8, 1, 32768, 128, 0, 128, None)
+    assert lib.baps_attention_fwd_split(*args, None, need, None) == 1
+    assert lib.baps_attention_fwd_split(*args, 4096, need - 1, None) == 1
+    assert lib.baps_attention_fwd_split(*args, 4096 + 16, need, None) == 1
+    assert lib.baps_attention_fwd_split(16, 16, 16, 16, None, 0, 32, 8, 1, 32768, 128, 0, 128, None, None, 0,
+                                        None) == 0                                      # empty work
 
 
 def test_codec_and_softmax_block_argument_checks(lib):
