@@ -17,7 +17,7 @@ using namespace baps;
 // in the low byte.  Lives in static device memory, one copy per device.
 __device__ uint32_t g_score_table[kTabEntries];
 // The compact code table of the fused attention kernels (see common.hpp).
-__device__ uint8_t g_code_table[kCodeEntries];
+__device__ __attribute__((aligned(256))) uint8_t g_code_table[kCodeTableBytes];
 
 // HiF8 value of a double, rounded once: truncating to fp32 toward zero keeps
 // the sign, the exponent and the leading mantissa bits that decide a
@@ -197,7 +197,7 @@ SplitPlan split_plan(int B, int Hq, int Hkv, int Sq, int Sk, int D, int block, i
     if (sp.nsplit < 2) return sp;
     sp.use = true;
     sp.nblk = nblk;
-    sp.bstride = (nblk + 63) / 64 * 64;
+    sp.bstride = (nblk + 255) / 256 * 256;
     const long long rows = (long long)B * Hkv * flat;
     long long off = 0;
     sp.off_acc = off;    off += align256(rows * nblk * (long long)block * 4);

@@ -215,7 +215,7 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void split_scores_kernel(SplitPara
 // ---------------------------------------------------------------------------
 // 2. pv: Alg. 1's per-block decisions up to the split, then P V of the split
 // ---------------------------------------------------------------------------
-constexpr int kWinBlocks = 64;       // block maxima per row and LDS window of the scan
+constexpr int kWinBlocks = 256;      // block maxima per LDS window of the scan (one row)
 
 template <int D, int BLK>
 struct PCfg {
@@ -236,9 +236,9 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void split_pv_kernel(SplitParams s
     constexpr int kDT = D / 16;
     constexpr int NT = PC::kThreads;
     constexpr int PS = PC::kPS;
-    __shared__ __attribute__((aligned(16))) uint8_t ctab[kCodeEntries];   // entry i at [i - kCodeLo]
+    __shared__ __attribute__((aligned(1024))) uint8_t ctab[kCodeTableBytes];   // entry i at [i - kCodeLo]
     __shared__ unsigned s_cnt[kRows][2];
-    __shared__ __attribute__((aligned(1024))) float s_win[KW][2][4 * kWinBlocks];   // scan windows
+    __shared__ __attribute__((aligned(1024))) float s_win[KW][2][kWinBlocks];       // scan windows
     __shared__ float refs_l[kRows * kSplitMaxBps];                                   // block references
     extern __shared__ __attribute__((aligned(1024))) char ring[];
     const uint32_t ring_lds = (uint32_t)(uintptr_t)LDS_PTR(char, ring);
@@ -262,18 +262,26 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void split_pv_kernel(SplitParams s
     const float ninf = -__builtin_huge_valf();
     const float c = p.c;
 
-    // -- block-maximum windows of the scan: one wave-wide 1 KiB DMA each, rows
-    //    4 * grp + (pass * KW + wave) of the tile, blocks [64 w, 64 w + 64)
+    // -- block-maximum windows of the scan: one wave-wide 1 KiB DMA each, the
+    //    maxima of blocks [256 w, 256 w + 256) of one row of the tile
     const uint32_t win_lds = (uint32_t)(uintptr_t)LDS_PTR(float, &s_win[wave][0][0]);
     const float* win = &s_win[wave][0][0];
     const int nwin = (j1 + kWinBlocks - 1) / kWinBlocks;
-    constexpr int kPasses = 4 / KW;
+    const int nr = min(kRows, flat - tile * kRows);         // rows of the tile (at least one)
+    const int npass = (nr + KW - 1) / KW;                   // the scan takes one row per wave at a time
     int ndma = 0;                                 // DMA ops of this wave issued so far
     int tag0 = 0, tag1 = 0;                       // ndma after the DMA of each window buffer
+    int tagc = 0;                                 // ndma after this wave's part of the code table
+    {
+        const uint32_t ctab_lds = (uint32_t)(uintptr_t)LDS_PTR(uint8_t, ctab);
+        for (int i = wave; i < kCodeTableBytes / 1024; i += KW) {
+            lds_dma_16(p.ctab + i * 1024 + 16 * lane, ctab_lds + (uint32_t)(i * 1024));
+            tagc = ++ndma;
+        }
+    }
     auto issue_win = [&](int pass, int w) {
-        const int srow = 4 * grp + pass * KW + wave;
-        const RowInfo wr = row_info(p, tile, g, srow);
-        const float* src = sp.bmax + (bg * flat + (wr.ok ? wr.f : 0)) * sp.bstride + w * kWinBlocks + 4 * c16;
+        const int srow = min(pass * KW + wave, nr - 1);
+        const float* src = sp.bmax + (bg * flat + tile * kRows + srow) * sp.bstride + w * kWinBlocks + 4 * lane;
         lds_dma_16(src, win_lds + (uint32_t)((w & 1) * 1024));
         ++ndma;
         if (w & 1) tag1 = ndma; else tag0 = ndma;
@@ -299,14 +307,14 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void split_pv_kernel(SplitParams s
     int issued = 0;
     for (; issued < min(nslots, RW); ++issued) issue_slot(issued);
 
-    // -- the scan: Alg. 1's decision for every block of [0, j1), 16 blocks
-    //    (one per lane of a 16-lane group) evaluated per step at the group's
-    //    current m; the blocks up to the first one that changes m are settled,
-    //    and the step repeats from there with the new m
+    // -- the scan: Alg. 1's decision for every block of [0, j1) of a row, 64
+    //    blocks (one per lane) evaluated per step at the current m; the blocks
+    //    up to the first one that changes m are settled, and the step repeats
+    //    from there with the new m (wave-uniform: a scalar register)
     const float lam = (float)p.lambda;
-    for (int pass = 0; pass < kPasses; ++pass) {
-        const int srow = 4 * grp + pass * KW + wave;
-        const RowInfo sr = row_info(p, tile, g, srow);
+    for (int pass = 0; pass < npass; ++pass) {
+        const int srow = pass * KW + wave;
+        const bool row_ok = srow < nr;
         float m = ninf;
         unsigned n_restart = 0, n_visit = 0;
         if (pass > 0) {                           // this pass's first windows (the V ring is already in flight)
@@ -315,18 +323,18 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void split_pv_kernel(SplitParams s
         }
         for (int w = 0; w < nwin; ++w) {
             wait_vm(ndma - ((w & 1) ? tag1 : tag0));
-            const float* wl = win + (w & 1) * 256 + grp * kWinBlocks;
+            const float* wl = win + (w & 1) * kWinBlocks;
 #pragma unroll 1
-            for (int kk = 0; kk < kWinBlocks / 16; ++kk) {
-                const int cb = w * kWinBlocks + 16 * kk;
+            for (int kk = 0; kk < kWinBlocks / 64; ++kk) {
+                const int cb = w * kWinBlocks + 64 * kk;
                 if (cb >= j1) break;
-                const int jb = cb + c16;
-                float amax = wl[16 * kk + c16];
-                if (!(sr.ok && jb < j1)) amax = ninf;
+                const int jb = cb + lane;
+                float amax = wl[64 * kk + lane];
+                if (!(row_ok && jb < j1)) amax = ninf;
                 const bool vis = amax != ninf;
                 const float ceil_ac = ceilf(amax * c);
                 const bool in_b0 = jb < p.n_b0;
-                const bool mine = sr.ok && jb >= j0 && jb < j1;
+                const bool mine = row_ok && jb >= j0 && jb < j1;
                 int lo = 0;
                 for (;;) {
                     const bool forced = in_b0 || (m == ninf);
@@ -335,37 +343,37 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void split_pv_kernel(SplitParams s
                     const float m_hi = __builtin_fmaxf(m, ceil_ac);
                     const float m_new = vis ? (restart ? m_hi : m + __builtin_fmaxf(0.0f, ceilf(tq))) : m;
                     const float ref_new = vis ? (restart ? m_hi : m) : ninf;
-                    const bool pend = c16 >= lo;
-                    const bool chg = pend && (hif8::f2u(m_new) != hif8::f2u(m));
-                    const unsigned long long bal = __ballot(chg);
-                    const uint32_t gm = (uint32_t)(bal >> (16 * grp)) & 0xffffu;
-                    const int f = gm ? __builtin_ctz(gm) : 16;
-                    if (pend && c16 <= f && mine) {
+                    const bool pend = lane >= lo;
+                    const unsigned long long bal = __ballot(pend && hif8::f2u(m_new) != hif8::f2u(m));
+                    const int f = bal ? (int)__builtin_ctzll(bal) : 64;
+                    if (pend && lane <= f && mine) {
                         refs_l[srow * kSplitMaxBps + (jb - j0)] = ref_new;   // -inf: no visible key
                         const bool b1 = vis && jb >= p.n_b0;
                         n_visit += b1 ? 1u : 0u;
                         n_restart += (b1 && restart) ? 1u : 0u;
                     }
-                    const float mf = __shfl(m_new, (lane & 48) + (f & 15), 64);
-                    m = f < 16 ? mf : m;
+                    if (f >= 63) {
+                        if (f == 63) m = __builtin_bit_cast(float, __builtin_amdgcn_readlane(
+                                              __builtin_bit_cast(int, m_new), 63));
+                        break;
+                    }
+                    m = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, m_new), f));
                     lo = f + 1;
-                    if (!__any(lo < 16)) break;
                 }
             }
             if (w + 2 < nwin) issue_win(pass, w + 2);
         }
 #pragma unroll
-        for (int o = 1; o < 16; o <<= 1) {
+        for (int o = 1; o < 64; o <<= 1) {
             n_visit += __shfl_xor(n_visit, o, 64);
             n_restart += __shfl_xor(n_restart, o, 64);
         }
-        if (c16 == 0) {
+        if (lane == 0 && row_ok) {
             s_cnt[srow][0] = n_restart;
             s_cnt[srow][1] = n_visit;
         }
     }
-
-    for (int i = tid; i < kCodeEntries; i += NT) ctab[i] = p.ctab[i];
+    wait_vm(ndma - tagc);                         // this wave's part of the code table has landed
 
     const RowInfo ri = row_info(p, tile, g, c16);
     const long long nkeys = (long long)sp.nblk * BLK;
@@ -489,7 +497,7 @@ __global__ __launch_bounds__(256) void split_combine_kernel(SplitParams sp)
     constexpr int QD = D / 4;                     // threads per split group (4 values of d each)
     constexpr int SG = 256 / QD;                  // split groups
     constexpr int PS = D + 4;
-    constexpr int kU = 4;                         // splits in flight per thread
+    constexpr int kU = 8;                         // splits in flight per thread
     __shared__ float red[256][6];
     const AttnParams& p = sp.a;
     const int tid = threadIdx.x;
@@ -508,19 +516,15 @@ __global__ __launch_bounds__(256) void split_combine_kernel(SplitParams sp)
         float rv[kU], dv[kU];
         f32x4 xv[kU];
 #pragma unroll
-        for (int u = 0; u < kU; ++u) {
-            const int s = s0 + u * SG;
-            if (s < sp.nsplit) {
-                const float* prow = pcol + s * pstride;
-                xv[u] = *reinterpret_cast<const f32x4*>(prow + 4 * q4);
-                dv[u] = prow[D];
-                rv[u] = prow[D + 1];
-            } else {
-                xv[u] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-                dv[u] = 0.0f;
-                rv[u] = ninf;
-            }
+        for (int u = 0; u < kU; ++u) {           // straight-line loads (a clamped split, masked below)
+            const float* prow = pcol + min(s0 + u * SG, sp.nsplit - 1) * pstride;
+            xv[u] = *reinterpret_cast<const f32x4*>(prow + 4 * q4);
+            dv[u] = prow[D];
+            rv[u] = prow[D + 1];
         }
+#pragma unroll
+        for (int u = 0; u < kU; ++u)
+            if (s0 + u * SG >= sp.nsplit) rv[u] = ninf;
 #pragma unroll
         for (int u = 0; u < kU; ++u) {
             if (rv[u] == ninf) continue;          // no visible key in that split

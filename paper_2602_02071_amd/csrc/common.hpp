@@ -34,6 +34,7 @@ constexpr int kTabShift = 19;
 constexpr int kCodeLo = 0x7A0;           // T = +2^-5
 constexpr int kCodeHi = 0x1840;          // T = -32
 constexpr int kCodeEntries = kCodeHi - kCodeLo + 1;
+constexpr int kCodeTableBytes = (kCodeEntries + 1023) / 1024 * 1024;   // device copy, zero-padded to whole KiB
 constexpr int kCodeBiasLog2 = 104;
 constexpr int kCodeMaxLambda = 8;
 
@@ -52,7 +53,7 @@ struct AttnParams {
     float* o;                   // [B, Hq, Sq, D]
     float* lse;                 // [B, Hq, Sq] or null
     const uint32_t* tab;        // score table (device)
-    const uint8_t* ctab;        // compact code table (device), kCodeEntries bytes
+    const uint8_t* ctab;        // compact code table (device), kCodeTableBytes bytes (entries, then zeros)
     unsigned long long* counters;  // [B*Hq][2] restarted / visited B1 row-blocks, or null
     int B, Hq, Hkv, Sq, Sk;
     int causal, lambda, n_b0;
@@ -85,7 +86,7 @@ struct SplitParams {
     float* acc;                 // [B*Hkv][flat][nblk*BLK] raw dot products q.k (-inf when masked)
     float* bmax;                // [B*Hkv][flat][bstride] raw row maximum of every key block
     float* part;                // [nsplit][B*Hkv][flat][D + 4] X, dX and the reference they are relative to
-    int nblk, bstride;          // key blocks, and the block-maximum row stride (a multiple of 64)
+    int nblk, bstride;          // key blocks, and the block-maximum row stride (a multiple of 256)
     int nsplit, bps;            // splits, blocks per split (at most kSplitMaxBps)
 };
 
