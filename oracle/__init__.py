@@ -87,6 +87,10 @@ def _load():
     L.orc_attention_ex.restype = i32
     L.orc_attention_ex.argtypes = [P, P, P, i32, i32, i32, i32, i32, i32, i32, i32,
                                    i32, i32, i32, i32, d, P, i64, P, P, P, P, d, ctypes.c_uint64, i32, i32]
+    L.orc_attention_tiles.restype = i32
+    L.orc_attention_tiles.argtypes = [P, P, P, i32, i32, i32, i32, i32, i32, i32, i32,
+                                      i32, i32, i32, i32, i32, i32, d, P, i64, P, P, P, P, P, d,
+                                      ctypes.c_uint64, i32]
     L.orc_exact_attention.restype = i32
     L.orc_exact_attention.argtypes = [P, P, P, i32, i32, i32, i32, i32, i32, i32,
                                       d, P, i64, P, P, i32]
@@ -189,7 +193,7 @@ def _rows(rows, total):
 
 def attention(q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, block, mode=E2E_HIF8, lam=1, n_b0=1,
               literal_else=False, scale_log2=0.0, rows=None, nthreads=0, margin=False, jitter=0.0,
-              jitter_seed=0, pv_bf16=False):
+              jitter_seed=0, pv_bf16=False, restart_rows=1, b0_last=False, visits=False):
     """Attention rows in one of the paper's setups.
 
     q: [B,Hq,Sq,D], k/v: [B,Hkv,Sk,D] bf16 bit patterns.  rows: global row
@@ -202,7 +206,14 @@ def attention(q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, block, mode=E2E_HIF8, lam=
     (same direction for jitter_seed 0, random signs otherwise).  pv_bf16 (the
     setups of eq. (2) only): P enters the P V product rounded to bf16, the
     input precision of a matrix unit, while the denominator sums P as
-    computed."""
+    computed.
+
+    restart_rows / b0_last / visits (Alg. 1 setups only) take the tile-level
+    path: the restart decision is shared by restart_rows consecutive query
+    positions of one head, B0 also holds each row's last key block when
+    b0_last, and the counts are per tile: restarts[n] (and, with visits,
+    one more array of visited B1 tile-blocks before the margin) hold the
+    row's tile's restarted B1 tile-blocks."""
     L = _load()
     q, k, v = _bits(q), _bits(k), _bits(v)
     rows = _rows(rows, B * Hq * Sq)
@@ -211,6 +222,17 @@ def attention(q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, block, mode=E2E_HIF8, lam=
     lse = np.zeros(n, dtype=np.float64)
     nrs = np.zeros(n, dtype=np.int32)
     mg = np.zeros(n, dtype=np.float64) if margin else None
+    if restart_rows != 1 or b0_last or visits:
+        nvs = np.zeros(n, dtype=np.int32)
+        st = L.orc_attention_tiles(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, Sq, Sk, D, int(causal), block,
+                                   int(mode), int(lam), int(n_b0), int(bool(b0_last)), int(restart_rows),
+                                   int(literal_else), float(scale_log2), _ptr(rows), n, _ptr(o), _ptr(lse),
+                                   _ptr(nrs), _ptr(nvs), _ptr(mg), float(jitter),
+                                   ctypes.c_uint64(int(jitter_seed)), int(nthreads))
+        if st:
+            raise ValueError("oracle rejected the attention arguments")
+        out = (o, lse, nrs) + ((nvs,) if visits else ()) + ((mg,) if margin else ())
+        return out
     st = L.orc_attention_ex(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, Sq, Sk, D, int(causal), block,
                             int(mode), int(lam), int(n_b0), int(literal_else), float(scale_log2),
                             _ptr(rows), n, _ptr(o), _ptr(lse), _ptr(nrs), _ptr(mg), float(jitter),

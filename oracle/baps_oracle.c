@@ -33,9 +33,11 @@
  *   R6  the integer row maximum uses ceil (Alg. 1).
  *   R7  the else-branch of Alg. 1 scales the new block by 2^(m~ - m) as well
  *       (the literal text leaves it unscaled; selectable for comparison).
- *   R8  the restart decision is taken per query row.
+ *   R8  the restart decision is taken per query row (per tile of query rows
+ *       in orc_attention_tiles, the paper-literal granularity).
  *   R9  a B0 block is a forced restart: T = S - m and P = E8(HiF8(T)).
- *   R10 B0 = the first n_b0 key blocks (n_b0 = 1), blocks visited in order.
+ *   R10 B0 = the first n_b0 key blocks (n_b0 = 1), blocks visited in order;
+ *       orc_attention_tiles can add each row's last (diagonal) key block.
  *   R11 causal masks are bottom-right aligned: query r sees keys
  *       c <= r + Sk - Sq; masked scores are -inf and drop out.
  *   R13 lse = ln2 * (m + log2 d), natural log of the softmax denominator.
@@ -802,6 +804,288 @@ int orc_attention(const uint16_t* q, const uint16_t* k, const uint16_t* v,
     return orc_attention_ex(q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, block, mode, lambda, n_b0,
                             literal_else, scale_log2, rows, nrows, o, lse, nrestart, NULL, 0.0, 0,
                             nthreads, 0);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Alg. 1 with the restart decision taken per tile of query rows             */
+/* ------------------------------------------------------------------------ */
+
+/* The paper decides a restart per tile: the tile of query rows restarts when
+ * the maximum entry of rowmax(T) over its rows exceeds lambda (Sec. 3.2,
+ * Alg. 1), and the restart rate is counted per tile (Sec. 4.3, Table 4).  A
+ * tile here is restart_rows consecutive query positions of one (batch,
+ * head); a B0 block forces the whole tile.  B0 is the first n_b0 key blocks
+ * and, with b0_last, also the last key block each row sees (the diagonal
+ * block under a causal mask; the text names the first and the last tiles as
+ * the critical ones).  Rows that see no key of a block take no part in its
+ * decision.  On a restart every row of the tile takes the high-precision
+ * path of Alg. 1 with its own row maximum; otherwise every row takes the
+ * 8-bit path with its own m.  Counters: B1 tile-blocks (a block that some
+ * row of the tile sees and that is in B0 for none of them) visited and
+ * restarted, the same for every row of the tile.  The margin of each row is
+ * the smallest decision margin over its whole tile, since any of them can
+ * move the shared decision. */
+typedef struct {
+    int R;                                  /* rows of the tile */
+    double **acc, **eps, **ot, **pv, **ref; /* per row: [keys], [keys], [D], [D], [blocks] */
+    double *m, *d, *tmax, *amax, *eps_blk, *mg;
+    int *kmax, *nblk;
+} tile_scratch;
+
+static void tile_alg1(const attn_job* J, int b0_last, int b, int h, int r0, int nr, tile_scratch* T,
+                      double* o, double* lse, int32_t* nrs, int32_t* nvis, double* margin)
+{
+    const int D = J->D, blk = J->block;
+    const int g = h / (J->Hq / J->Hkv);
+    const uint16_t* kb = J->k + ((int64_t)b * J->Hkv + g) * (int64_t)J->Sk * D;
+    const uint16_t* vb = J->v + ((int64_t)b * J->Hkv + g) * (int64_t)J->Sk * D;
+    const int exact = (J->mode == ORC_E2E_EXACT);
+    int nblk_t = 0;
+    for (int i = 0; i < nr; ++i) {
+        const int r = r0 + i;
+        const uint16_t* qr = J->q + (((int64_t)b * J->Hq + h) * J->Sq + r) * D;
+        const uint64_t rowid = (((uint64_t)b * J->Hq + h) * J->Sq + r);
+        T->kmax[i] = last_visible_key(J, r);
+        T->nblk[i] = T->kmax[i] < 0 ? 0 : T->kmax[i] / blk + 1;
+        if (T->nblk[i] > nblk_t) nblk_t = T->nblk[i];
+        T->m[i] = -INFINITY;
+        T->d[i] = 0.0;
+        T->mg[i] = INFINITY;
+        for (int x = 0; x < D; ++x) T->ot[i][x] = 0.0;
+        for (int c = 0; c <= T->kmax[i]; ++c) {                          /* as in row_alg1 */
+            const uint16_t* kr = kb + (int64_t)c * D;
+            double a = dot64(qr, kr, D);
+            const double e_acc = ACC_ERR * ldexp(abs_dot64(qr, kr, D), -24);
+            if (J->jitter != 0.0) {
+                double sgn = 1.0;
+                if (J->jitter_seed)
+                    sgn = (splitmix64(J->jitter_seed ^ (rowid * 1000003ull + (uint64_t)c)) & 1) ? 1.0 : -1.0;
+                a += J->jitter * sgn * e_acc;
+            }
+            T->acc[i][c] = exact ? a : (double)(float)a;
+            T->eps[i][c] = e_acc * J->c64;
+        }
+    }
+    int32_t t_restart = 0, t_visit = 0;
+    double tile_mg = INFINITY;
+    for (int j = 0; j < nblk_t; ++j) {
+        /* the tile's decision: any visible row in B0, or any visible row whose
+         * 8-bit rowmax(T) (at its own m) exceeds lambda */
+        int any_vis = 0, any_b0 = 0, restart = 0;
+        for (int i = 0; i < nr; ++i) {
+            if (j >= T->nblk[i]) continue;
+            any_vis = 1;
+            const int c0 = j * blk, c1 = (c0 + blk <= T->kmax[i] + 1) ? c0 + blk : T->kmax[i] + 1;
+            double amax = -INFINITY, eb = 0.0, tmax = -INFINITY;
+            for (int c = c0; c < c1; ++c) {
+                if (T->acc[i][c] > amax) amax = T->acc[i][c];
+                if (T->eps[i][c] > eb) eb = T->eps[i][c];
+                double t;
+                if (exact) t = T->acc[i][c] * J->c64 - T->m[i];
+                else t = orc_hif8_round((double)fmaf((float)T->acc[i][c], J->c32, (float)(-T->m[i])), 1);
+                if (t > tmax) tmax = t;
+            }
+            T->amax[i] = amax;
+            T->eps_blk[i] = eb;
+            T->tmax[i] = tmax;
+            const int in_b0 = j < J->n_b0 || (b0_last && j == T->nblk[i] - 1);
+            if (in_b0) {
+                any_b0 = 1;
+                restart = 1;
+            } else {
+                if (ceil(tmax) > (double)J->lambda) restart = 1;
+                if (T->m[i] != -INFINITY) {
+                    double dist = hif8_boundary_distance(amax * J->c64 - T->m[i]) / eb;
+                    if (dist < tile_mg) tile_mg = dist;
+                }
+            }
+        }
+        if (!any_vis) continue;
+        if (!any_b0) {
+            ++t_visit;
+            if (restart) ++t_restart;
+        }
+        for (int i = 0; i < nr; ++i) {
+            if (j >= T->nblk[i]) continue;
+            const int c0 = j * blk, c1 = (c0 + blk <= T->kmax[i] + 1) ? c0 + blk : T->kmax[i] + 1;
+            const double m = T->m[i];
+            double m_new, ref;
+            if (restart) {
+                double M = -INFINITY;
+                for (int c = c0; c < c1; ++c) {
+                    double sv = exact ? T->acc[i][c] * J->c64 : (double)((float)T->acc[i][c] * J->c32);
+                    if (sv > M) M = sv;
+                }
+                m_new = fmax(m, ceil(M));
+                ref = m_new;
+                double dist = integer_distance(T->amax[i] * J->c64) / T->eps_blk[i];
+                if (dist < tile_mg) tile_mg = dist;
+            } else {
+                m_new = m + fmax(0.0, ceil(T->tmax[i]));
+                ref = m;
+            }
+            double rowsum = 0.0;
+            for (int x = 0; x < D; ++x) T->pv[i][x] = 0.0;
+            for (int c = c0; c < c1; ++c) {
+                double p;
+                if (exact) p = exp2(T->acc[i][c] * J->c64 - ref);
+                else p = e8_hif8(orc_hif8_round((double)fmaf((float)T->acc[i][c], J->c32, (float)(-ref)), 1));
+                if (p == 0.0) continue;
+                rowsum += p;
+                const uint16_t* vr = vb + (int64_t)c * D;
+                for (int x = 0; x < D; ++x) T->pv[i][x] += p * bf16_to_double(vr[x]);
+            }
+            const double alpha = (m == -INFINITY) ? 0.0 : exp2(m - m_new);
+            const double beta = (J->literal_else && !restart) ? 1.0 : exp2(ref - m_new);
+            T->d[i] = alpha * T->d[i] + beta * rowsum;
+            for (int x = 0; x < D; ++x) T->ot[i][x] = alpha * T->ot[i][x] + beta * T->pv[i][x];
+            T->m[i] = m_new;
+            T->ref[i][j] = ref;
+        }
+    }
+    if (margin && !exact) {
+        /* the HiF8 rounding of every T with weight >= 2^-12 of its row's maximum */
+        for (int i = 0; i < nr; ++i) {
+            for (int j = 0; j < T->nblk[i]; ++j) {
+                const int c0 = j * blk, c1 = (c0 + blk <= T->kmax[i] + 1) ? c0 + blk : T->kmax[i] + 1;
+                for (int c = c0; c < c1; ++c) {
+                    double x = T->acc[i][c] * J->c64 - T->ref[i][j];
+                    double p = e8_hif8(orc_hif8_round((double)fmaf((float)T->acc[i][c], J->c32,
+                                                                   (float)(-T->ref[i][j])), 1));
+                    if (ldexp(p, (int)(T->ref[i][j] - T->m[i])) < 1.0 / 4096.0) continue;
+                    double dist = hif8_boundary_distance(x) / T->eps[i][c];
+                    if (dist < tile_mg) tile_mg = dist;
+                }
+            }
+        }
+    }
+    for (int i = 0; i < nr; ++i) {
+        if (T->nblk[i] == 0) {
+            for (int x = 0; x < D; ++x) o[(int64_t)i * D + x] = 0.0;
+            lse[i] = -INFINITY;
+        } else {
+            for (int x = 0; x < D; ++x) o[(int64_t)i * D + x] = T->ot[i][x] / T->d[i];
+            lse[i] = M_LN2 * (T->m[i] + log2(T->d[i]));
+        }
+        nrs[i] = t_restart;
+        nvis[i] = t_visit;
+        if (margin) margin[i] = exact ? INFINITY : tile_mg;
+    }
+}
+
+typedef struct {
+    attn_job* J;
+    int R, b0_last;
+    const int64_t* tiles;       /* unique tile keys (b*Hq + h)*ntq + t, ascending */
+    const int64_t* first;       /* [ntiles+1] ranges into order[] */
+    const int64_t* order;       /* requested-row indices sorted by tile */
+    int32_t* nvisit;
+} tiles_ctx;
+
+static void tiles_range(void* p, int64_t t0, int64_t t1)
+{
+    tiles_ctx* C = (tiles_ctx*)p;
+    attn_job* J = C->J;
+    const int D = J->D, R = C->R;
+    const int64_t ntq = (J->Sq + R - 1) / R;
+    const size_t nkeys = (size_t)(J->Sk > J->block ? J->Sk : J->block) + 1;
+    const size_t nblk = (size_t)(J->Sk / J->block) + 2;
+    tile_scratch T;
+    T.R = R;
+    T.acc = (double**)malloc(sizeof(double*) * R); T.eps = (double**)malloc(sizeof(double*) * R);
+    T.ot = (double**)malloc(sizeof(double*) * R); T.pv = (double**)malloc(sizeof(double*) * R);
+    T.ref = (double**)malloc(sizeof(double*) * R);
+    for (int i = 0; i < R; ++i) {
+        T.acc[i] = (double*)malloc(sizeof(double) * nkeys); T.eps[i] = (double*)malloc(sizeof(double) * nkeys);
+        T.ot[i] = (double*)malloc(sizeof(double) * D); T.pv[i] = (double*)malloc(sizeof(double) * D);
+        T.ref[i] = (double*)malloc(sizeof(double) * nblk);
+    }
+    T.m = (double*)malloc(sizeof(double) * R); T.d = (double*)malloc(sizeof(double) * R);
+    T.tmax = (double*)malloc(sizeof(double) * R); T.amax = (double*)malloc(sizeof(double) * R);
+    T.eps_blk = (double*)malloc(sizeof(double) * R); T.mg = (double*)malloc(sizeof(double) * R);
+    T.kmax = (int*)malloc(sizeof(int) * R); T.nblk = (int*)malloc(sizeof(int) * R);
+    double* o = (double*)malloc(sizeof(double) * (size_t)R * D);
+    double* lse = (double*)malloc(sizeof(double) * R);
+    double* mg = (double*)malloc(sizeof(double) * R);
+    int32_t* nrs = (int32_t*)malloc(sizeof(int32_t) * R);
+    int32_t* nvs = (int32_t*)malloc(sizeof(int32_t) * R);
+    for (int64_t t = t0; t < t1; ++t) {
+        const int64_t key = C->tiles[t];
+        const int tq = (int)(key % ntq);
+        const int h = (int)((key / ntq) % J->Hq);
+        const int b = (int)(key / (ntq * J->Hq));
+        const int r0 = tq * R;
+        const int nr = (r0 + R <= J->Sq) ? R : J->Sq - r0;
+        tile_alg1(J, C->b0_last, b, h, r0, nr, &T, o, lse, nrs, nvs, J->margin ? mg : NULL);
+        for (int64_t e = C->first[t]; e < C->first[t + 1]; ++e) {
+            const int64_t i = C->order[e];
+            const int r = (int)(J->rows[i] % J->Sq) - r0;
+            for (int x = 0; x < D; ++x) J->o[i * D + x] = o[(int64_t)r * D + x];
+            J->lse[i] = lse[r];
+            if (J->nrestart) J->nrestart[i] = nrs[r];
+            if (C->nvisit) C->nvisit[i] = nvs[r];
+            if (J->margin) J->margin[i] = mg[r];
+        }
+    }
+    for (int i = 0; i < R; ++i) { free(T.acc[i]); free(T.eps[i]); free(T.ot[i]); free(T.pv[i]); free(T.ref[i]); }
+    free(T.acc); free(T.eps); free(T.ot); free(T.pv); free(T.ref);
+    free(T.m); free(T.d); free(T.tmax); free(T.amax); free(T.eps_blk); free(T.mg); free(T.kmax); free(T.nblk);
+    free(o); free(lse); free(mg); free(nrs); free(nvs);
+}
+
+static int64_t* g_sort_keys;            /* qsort context (single-threaded section) */
+static int cmp_by_key(const void* a, const void* b)
+{
+    const int64_t ka = g_sort_keys[*(const int64_t*)a], kb = g_sort_keys[*(const int64_t*)b];
+    return ka < kb ? -1 : (ka > kb ? 1 : 0);
+}
+
+/* Alg. 1 with tile-level restart (restart_rows >= 1 query positions per
+ * tile) and optionally B0 = {first n_b0 blocks, each row's last block}.
+ * Modes ORC_E2E_HIF8 and ORC_E2E_EXACT.  Besides the outputs of
+ * orc_attention_ex: nvisit (nullable), the visited B1 tile-blocks of each
+ * requested row's tile; nrestart holds the restarted ones.  Returns 0 or 1. */
+int orc_attention_tiles(const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                        int B, int Hq, int Hkv, int Sq, int Sk, int D, int causal, int block,
+                        int mode, int lambda, int n_b0, int b0_last, int restart_rows, int literal_else,
+                        double scale_log2, const int64_t* rows, int64_t nrows, double* o, double* lse,
+                        int32_t* nrestart, int32_t* nvisit, double* margin, double jitter,
+                        uint64_t jitter_seed, int nthreads)
+{
+    if (attn_check(B, Hq, Hkv, Sq, Sk, D, block)) return 1;
+    if ((mode != ORC_E2E_HIF8 && mode != ORC_E2E_EXACT) || restart_rows < 1 || n_b0 < 0) return 1;
+    attn_job J = { q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, block, mode, lambda, n_b0,
+                   literal_else, 0.0f, 0.0, rows, o, lse, nrestart, margin, jitter, jitter_seed, 0 };
+    J.c64 = scale_log2 != 0.0 ? scale_log2 : M_LOG2E / sqrt((double)D);
+    J.c32 = (float)J.c64;
+    if (mode != ORC_E2E_EXACT) J.c64 = (double)J.c32;
+    if (nrows == 0) return 0;
+    const int R = restart_rows;
+    const int64_t ntq = (Sq + R - 1) / R;
+    int64_t* key = (int64_t*)malloc(sizeof(int64_t) * nrows);
+    int64_t* order = (int64_t*)malloc(sizeof(int64_t) * nrows);
+    int64_t* tiles = (int64_t*)malloc(sizeof(int64_t) * nrows);
+    int64_t* first = (int64_t*)malloc(sizeof(int64_t) * (nrows + 1));
+    for (int64_t i = 0; i < nrows; ++i) {
+        const int64_t g = rows[i];
+        key[i] = (g / Sq) * ntq + (g % Sq) / R;
+        order[i] = i;
+    }
+    g_sort_keys = key;
+    qsort(order, (size_t)nrows, sizeof(int64_t), cmp_by_key);
+    int64_t nt = 0;
+    for (int64_t e = 0; e < nrows; ++e) {
+        if (e == 0 || key[order[e]] != key[order[e - 1]]) {
+            tiles[nt] = key[order[e]];
+            first[nt] = e;
+            ++nt;
+        }
+    }
+    first[nt] = nrows;
+    tiles_ctx C = { &J, R, b0_last ? 1 : 0, tiles, first, order, nvisit };
+    parallel_for(nt, nthreads, 1, tiles_range, &C);
+    free(key); free(order); free(tiles); free(first);
+    return 0;
 }
 
 int orc_exact_attention(const uint16_t* q, const uint16_t* k, const uint16_t* v,
