@@ -80,10 +80,21 @@ typedef struct {
     int lambda;                          /* restart threshold (integer, Alg. 1); 1 canonical  */
     int n_b0;                            /* key blocks in B0 (taken first, Alg. 1); 1 canonical */
     float scale_log2;                    /* score scale in log2 units; 0 => log2(e)/sqrt(D)    */
-    unsigned long long* restart_counts;  /* device [B*Hq][2]: restarted and visited B1 row-
-                                            blocks (accumulated with atomics; the caller
-                                            zeroes it); NULL to skip                          */
+    unsigned long long* restart_counts;  /* device [B*Hq][2]: restarted and visited B1 tile-
+                                            blocks (a tile is one query row unless
+                                            restart_rows > 1; accumulated with atomics; the
+                                            caller zeroes it); NULL to skip                   */
     int mode;                            /* BAPS_MODE_*; anything else is an invalid argument  */
+    int restart_rows;                    /* query positions of one head that share the restart
+                                            decision (the paper's tile, Sec. 3.2); 0 or 1 per
+                                            row (canonical).  E2E setup only; a power of two
+                                            with restart_rows * (Hq/Hkv) <= 256 and Hq/Hkv a
+                                            power of two <= 32, else BAPS_UNSUPPORTED          */
+    int b0_last;                         /* nonzero: B0 also holds each row's last visible key
+                                            block (the diagonal block when causal)            */
+    unsigned long long* tile_counts;     /* device [B*Hq][ceil(Sq/restart_rows)][2]: restarted
+                                            and visited B1 blocks per tile (Table 4's restart
+                                            rates); caller-zeroed, NULL to skip               */
 } baps_params_t;
 
 /* baps_attention_fwd with explicit knobs; p must not be NULL; scale_log2

@@ -35,7 +35,8 @@ class BapsError(RuntimeError):
 
 class baps_params_t(ctypes.Structure):
     _fields_ = [("lambda_", ctypes.c_int), ("n_b0", ctypes.c_int), ("scale_log2", ctypes.c_float),
-                ("restart_counts", ctypes.c_void_p), ("mode", ctypes.c_int)]
+                ("restart_counts", ctypes.c_void_p), ("mode", ctypes.c_int), ("restart_rows", ctypes.c_int),
+                ("b0_last", ctypes.c_int), ("tile_counts", ctypes.c_void_p)]
 
 
 # softmax setups (include/baps.h)
@@ -112,24 +113,31 @@ def baps_attention_fwd(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, st
         _p(q), _p(k), _p(v), _p(o), _p(lse), B, Hq, Hkv, Sq, Sk, D, int(causal), block, _stream(stream)))
 
 
+def _params(lam=1, n_b0=1, scale_log2=0.0, restart_counts=None, mode=BAPS_MODE_E2E_HIF8, restart_rows=1,
+            b0_last=False, tile_counts=None):
+    return baps_params_t(int(lam), int(n_b0), float(scale_log2), _p(restart_counts), int(mode), int(restart_rows),
+                         int(bool(b0_last)), _p(tile_counts))
+
+
 def baps_attention_fwd_ex(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, lam=1, n_b0=1,
-                          scale_log2=0.0, restart_counts=None, stream=None, mode=BAPS_MODE_E2E_HIF8):
-    prm = baps_params_t(int(lam), int(n_b0), float(scale_log2), _p(restart_counts), int(mode))
+                          scale_log2=0.0, restart_counts=None, stream=None, mode=BAPS_MODE_E2E_HIF8,
+                          restart_rows=1, b0_last=False, tile_counts=None):
+    prm = _params(lam, n_b0, scale_log2, restart_counts, mode, restart_rows, b0_last, tile_counts)
     _check("baps_attention_fwd_ex", load().baps_attention_fwd_ex(
         _p(q), _p(k), _p(v), _p(o), _p(lse), B, Hq, Hkv, Sq, Sk, D, int(causal), block,
         ctypes.byref(prm), _stream(stream)))
 
 
 def baps_attention_split_workspace(B, Hq, Hkv, Sq, Sk, D, block, lam=1, n_b0=1, scale_log2=0.0,
-                                   mode=BAPS_MODE_E2E_HIF8):
-    prm = baps_params_t(int(lam), int(n_b0), float(scale_log2), None, int(mode))
+                                   mode=BAPS_MODE_E2E_HIF8, restart_rows=1, b0_last=False):
+    prm = _params(lam, n_b0, scale_log2, None, mode, restart_rows, b0_last)
     return int(load().baps_attention_split_workspace(B, Hq, Hkv, Sq, Sk, D, block, ctypes.byref(prm)))
 
 
 def baps_attention_fwd_split(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, workspace, workspace_bytes,
                              lam=1, n_b0=1, scale_log2=0.0, restart_counts=None, stream=None,
-                             mode=BAPS_MODE_E2E_HIF8):
-    prm = baps_params_t(int(lam), int(n_b0), float(scale_log2), _p(restart_counts), int(mode))
+                             mode=BAPS_MODE_E2E_HIF8, restart_rows=1, b0_last=False, tile_counts=None):
+    prm = _params(lam, n_b0, scale_log2, restart_counts, mode, restart_rows, b0_last, tile_counts)
     _check("baps_attention_fwd_split", load().baps_attention_fwd_split(
         _p(q), _p(k), _p(v), _p(o), _p(lse), B, Hq, Hkv, Sq, Sk, D, int(causal), block,
         ctypes.byref(prm), _p(workspace), int(workspace_bytes), _stream(stream)))
@@ -162,10 +170,12 @@ def baps_init():
 
 # ------------------------------------------------------------ tensor helpers
 def attention(q, k, v, causal, block, lse=True, lam=None, n_b0=None, scale_log2=0.0, restart_counts=None,
-              stream=None, mode=BAPS_MODE_E2E_HIF8, split=False):
+              stream=None, mode=BAPS_MODE_E2E_HIF8, split=False, restart_rows=1, b0_last=False, tile_counts=None):
     """Allocate O (and lse) with torch on q's device and run the fused pass.
     q [B,Hq,Sq,D], k/v [B,Hkv,Sk,D] bf16 CUDA tensors, contiguous.  split:
-    take baps_attention_fwd_split, with a workspace allocated here."""
+    take baps_attention_fwd_split, with a workspace allocated here.
+    restart_rows / b0_last / tile_counts: the tile-level restart knobs of
+    baps_params_t."""
     import torch
     B, Hq, Sq, D = q.shape
     Hkv, Sk = k.shape[1], k.shape[2]
@@ -176,14 +186,16 @@ def attention(q, k, v, causal, block, lse=True, lam=None, n_b0=None, scale_log2=
     l = torch.empty((B, Hq, Sq), dtype=torch.float32, device=q.device) if lse else None
     if split:
         lam_, nb_ = 1 if lam is None else lam, 1 if n_b0 is None else n_b0
-        nbytes = baps_attention_split_workspace(B, Hq, Hkv, Sq, Sk, D, block, lam_, nb_, scale_log2, mode)
+        nbytes = baps_attention_split_workspace(B, Hq, Hkv, Sq, Sk, D, block, lam_, nb_, scale_log2, mode,
+                                                restart_rows, b0_last)
         ws = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=q.device)
         baps_attention_fwd_split(q, k, v, o, l, B, Hq, Hkv, Sq, Sk, D, causal, block, ws, nbytes, lam_, nb_,
-                                 scale_log2, restart_counts, stream, mode)
-    elif lam is None and n_b0 is None and not scale_log2 and restart_counts is None and mode == BAPS_MODE_E2E_HIF8:
+                                 scale_log2, restart_counts, stream, mode, restart_rows, b0_last, tile_counts)
+    elif (lam is None and n_b0 is None and not scale_log2 and restart_counts is None and mode == BAPS_MODE_E2E_HIF8
+          and restart_rows == 1 and not b0_last and tile_counts is None):
         baps_attention_fwd(q, k, v, o, l, B, Hq, Hkv, Sq, Sk, D, causal, block, stream)
     else:
         baps_attention_fwd_ex(q, k, v, o, l, B, Hq, Hkv, Sq, Sk, D, causal, block,
                               1 if lam is None else lam, 1 if n_b0 is None else n_b0, scale_log2,
-                              restart_counts, stream, mode)
+                              restart_counts, stream, mode, restart_rows, b0_last, tile_counts)
     return o, l

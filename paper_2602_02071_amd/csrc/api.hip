@@ -127,40 +127,99 @@ int table_on_current_device(const uint32_t** out, const uint8_t** code = nullptr
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 
-int attention_impl(const void* q, const void* k, const void* v, float* o, float* lse, int B, int Hq,
-                   int Hkv, int Sq, int Sk, int D, int causal, int block, int lambda, int n_b0,
-                   float scale_log2, unsigned long long* counters, int mode, void* stream)
+// Canonical knobs when the caller passes none.
+baps_params_t knobs_of(const baps_params_t* prm)
 {
+    if (prm) return *prm;
+    baps_params_t k;
+    std::memset(&k, 0, sizeof(k));
+    k.lambda = 1;
+    k.n_b0 = 1;
+    k.mode = BAPS_MODE_E2E_HIF8;
+    return k;
+}
+
+bool pow2(long long x) { return x > 0 && (x & (x - 1)) == 0; }
+
+// The tile height the kernels use: one row per tile unless restart_rows > 1
+// and Sq > 1; a tile taller than the query rows is the same single tile as
+// the smallest power of two >= Sq.
+int effective_rows(int R, int Sq)
+{
+    if (R <= 1 || Sq <= 1) return 1;
+    long long p2 = 1;
+    while (p2 < Sq) p2 <<= 1;
+    return (int)(R < p2 ? R : p2);
+}
+
+// Argument checks and the launch descriptor shared by the one-pass and the
+// split-key paths (no HIP call; the device tables are attached by
+// attach_tables); returns a status (BAPS_OK with *empty set: nothing to do).
+int make_params(const void* q, const void* k, const void* v, float* o, float* lse, int B, int Hq, int Hkv,
+                int Sq, int Sk, int D, int causal, int block, const baps_params_t& kn, AttnParams* out,
+                bool* empty)
+{
+    *empty = false;
+    const int mode = kn.mode;
     if (mode != BAPS_MODE_E2E_HIF8 && mode != BAPS_MODE_DEFAULT && mode != BAPS_MODE_EXP2_HIF8)
         return BAPS_INVALID_ARGUMENT;
-    if (B < 0 || Hq < 0 || Hkv < 0 || Sq < 0 || Sk < 0 || n_b0 < 0) return BAPS_INVALID_ARGUMENT;
-    if (!(scale_log2 >= 0.0f) || std::isinf(scale_log2)) return BAPS_INVALID_ARGUMENT;
-    if (B == 0 || Hq == 0 || Sq == 0) return BAPS_OK;
+    if (B < 0 || Hq < 0 || Hkv < 0 || Sq < 0 || Sk < 0 || kn.n_b0 < 0 || kn.restart_rows < 0)
+        return BAPS_INVALID_ARGUMENT;
+    if (!(kn.scale_log2 >= 0.0f) || std::isinf(kn.scale_log2)) return BAPS_INVALID_ARGUMENT;
+    if (B == 0 || Hq == 0 || Sq == 0) {
+        *empty = true;
+        return BAPS_OK;
+    }
     if (Hkv == 0 || Hq % Hkv != 0) return BAPS_INVALID_ARGUMENT;
     if (!q || !o || (Sk > 0 && (!k || !v))) return BAPS_INVALID_ARGUMENT;
     if (!aligned16(q) || !aligned16(o) || (Sk > 0 && (!aligned16(k) || !aligned16(v))))
         return BAPS_INVALID_ARGUMENT;
     if (!(D == 64 || D == 128) || !(block == 32 || block == 64 || block == 128)) return BAPS_UNSUPPORTED;
     if ((long long)Sq * (Hq / Hkv) > 0x7fffffffLL || Hkv > 65535 || B > 65535) return BAPS_UNSUPPORTED;
-    const uint32_t* tab = nullptr;
-    const uint8_t* ctab = nullptr;
-    int st = table_on_current_device(&tab, &ctab);
-    if (st) return st;
-    AttnParams p;
-    p.ctab = ctab;
+    const int G = Hq / Hkv;
+    if (kn.restart_rows > 1 && !pow2(kn.restart_rows)) return BAPS_UNSUPPORTED;
+    const int R = effective_rows(kn.restart_rows, Sq);
+    if (R > 1 && (mode != BAPS_MODE_E2E_HIF8 || !pow2(G) || G > 32 || (long long)R * G > 256))
+        return BAPS_UNSUPPORTED;
+    AttnParams& p = *out;
+    p.tab = nullptr;
+    p.ctab = nullptr;
     p.q = static_cast<const uint16_t*>(q);
     p.k = static_cast<const uint16_t*>(k);
     p.v = static_cast<const uint16_t*>(v);
     p.o = o;
     p.lse = lse;
-    p.tab = tab;
-    p.counters = counters;
+    p.counters = kn.restart_counts;
+    p.tile_counts = kn.tile_counts;
     p.B = B; p.Hq = Hq; p.Hkv = Hkv; p.Sq = Sq; p.Sk = Sk;
     p.causal = causal ? 1 : 0;
-    p.lambda = lambda;
-    p.n_b0 = n_b0;
+    p.lambda = kn.lambda;
+    p.n_b0 = kn.n_b0;
     p.mode = mode;
-    p.c = scale_log2 > 0.0f ? scale_log2 : (float)(1.4426950408889634 / std::sqrt((double)D));
+    p.restart_rows = R;
+    p.b0_last = kn.b0_last ? 1 : 0;
+    p.c = kn.scale_log2 > 0.0f ? kn.scale_log2 : (float)(1.4426950408889634 / std::sqrt((double)D));
+    return BAPS_OK;
+}
+
+int attach_tables(AttnParams* p)
+{
+    const uint32_t* tab = nullptr;
+    const uint8_t* ctab = nullptr;
+    const int st = table_on_current_device(&tab, &ctab);
+    p->tab = tab;
+    p->ctab = ctab;
+    return st;
+}
+
+int attention_impl(const void* q, const void* k, const void* v, float* o, float* lse, int B, int Hq,
+                   int Hkv, int Sq, int Sk, int D, int causal, int block, const baps_params_t& kn, void* stream)
+{
+    AttnParams p;
+    bool empty = false;
+    int st = make_params(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, kn, &p, &empty);
+    if (st || empty) return st;
+    if ((st = attach_tables(&p))) return st;
     clear_stale_error();
     return status_of(launch_attention(p, D, block, static_cast<hipStream_t>(stream)));
 }
@@ -176,12 +235,13 @@ struct SplitPlan {
 
 long long align256(long long x) { return (x + 255) & ~255LL; }
 
-SplitPlan split_plan(int B, int Hq, int Hkv, int Sq, int Sk, int D, int block, int lambda, int mode)
+SplitPlan split_plan(int B, int Hq, int Hkv, int Sq, int Sk, int D, int block, const baps_params_t& kn)
 {
     SplitPlan sp;
     if (B <= 0 || Hq <= 0 || Hkv <= 0 || Sq <= 0 || Sk <= 0 || Hq % Hkv) return sp;
     if (!(D == 64 || D == 128) || !(block == 32 || block == 64 || block == 128)) return sp;
-    if (mode != BAPS_MODE_E2E_HIF8 || lambda > kCodeMaxLambda) return sp;
+    if (kn.mode != BAPS_MODE_E2E_HIF8 || kn.lambda > kCodeMaxLambda) return sp;
+    if (kn.restart_rows < 0 || effective_rows(kn.restart_rows, Sq) > 1) return sp;   // per-row decisions only
     const long long flat = (long long)Sq * (Hq / Hkv);
     if (flat > 64) return sp;                                   // the prefill kernel's regime
     const long long tiles = (flat + 15) / 16;
@@ -214,9 +274,7 @@ extern "C" {
 long long baps_attention_split_workspace(int B, int Hq, int Hkv, int Sq, int Sk, int D, int block,
                                          const baps_params_t* prm)
 {
-    const int lambda = prm ? prm->lambda : 1;
-    const int mode = prm ? prm->mode : BAPS_MODE_E2E_HIF8;
-    const SplitPlan sp = split_plan(B, Hq, Hkv, Sq, Sk, D, block, lambda, mode);
+    const SplitPlan sp = split_plan(B, Hq, Hkv, Sq, Sk, D, block, knobs_of(prm));
     return sp.use ? sp.bytes : 0;
 }
 
@@ -225,40 +283,15 @@ int baps_attention_fwd_split(const void* q, const void* k, const void* v, float*
                              void* workspace, long long workspace_bytes, void* stream)
 {
     try {
-        const int lambda = prm ? prm->lambda : 1;
-        const int n_b0 = prm ? prm->n_b0 : 1;
-        const float scale_log2 = prm ? prm->scale_log2 : 0.0f;
-        unsigned long long* counters = prm ? prm->restart_counts : nullptr;
-        const int mode = prm ? prm->mode : BAPS_MODE_E2E_HIF8;
-        const SplitPlan plan = split_plan(B, Hq, Hkv, Sq, Sk, D, block, lambda, mode);
-        if (!plan.use)
-            return attention_impl(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, lambda, n_b0,
-                                  scale_log2, counters, mode, stream);
-        // the same argument checks as the one-pass path (they pass or fail alike)
-        if (n_b0 < 0 || !(scale_log2 >= 0.0f) || std::isinf(scale_log2)) return BAPS_INVALID_ARGUMENT;
-        if (!q || !o || !k || !v) return BAPS_INVALID_ARGUMENT;
-        if (!aligned16(q) || !aligned16(o) || !aligned16(k) || !aligned16(v)) return BAPS_INVALID_ARGUMENT;
-        if (!workspace || workspace_bytes < plan.bytes || ((uintptr_t)workspace & 255u)) return BAPS_INVALID_ARGUMENT;
-        const uint32_t* tab = nullptr;
-        const uint8_t* ctab = nullptr;
-        int st = table_on_current_device(&tab, &ctab);
-        if (st) return st;
+        const baps_params_t kn = knobs_of(prm);
+        const SplitPlan plan = split_plan(B, Hq, Hkv, Sq, Sk, D, block, kn);
+        if (!plan.use) return attention_impl(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, kn, stream);
         SplitParams sp;
-        AttnParams& p = sp.a;
-        p.q = static_cast<const uint16_t*>(q);
-        p.k = static_cast<const uint16_t*>(k);
-        p.v = static_cast<const uint16_t*>(v);
-        p.o = o;
-        p.lse = lse;
-        p.tab = tab;
-        p.ctab = ctab;
-        p.counters = counters;
-        p.B = B; p.Hq = Hq; p.Hkv = Hkv; p.Sq = Sq; p.Sk = Sk;
-        p.causal = causal ? 1 : 0;
-        p.lambda = lambda;
-        p.n_b0 = n_b0;
-        p.mode = mode;
-        p.c = scale_log2 > 0.0f ? scale_log2 : (float)(1.4426950408889634 / std::sqrt((double)D));
+        bool empty = false;
+        int st = make_params(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, kn, &sp.a, &empty);
+        if (st || empty) return st;
+        if (!workspace || workspace_bytes < plan.bytes || ((uintptr_t)workspace & 255u)) return BAPS_INVALID_ARGUMENT;
+        if ((st = attach_tables(&sp.a))) return st;
         char* ws = static_cast<char*>(workspace);
         sp.acc = reinterpret_cast<float*>(ws + plan.off_acc);
         sp.bmax = reinterpret_cast<float*>(ws + plan.off_bmax);
@@ -278,8 +311,7 @@ int baps_attention_fwd(const void* q, const void* k, const void* v, float* o, fl
                        int Hkv, int Sq, int Sk, int D, int causal, int block, void* stream)
 {
     try {
-        return attention_impl(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, 1, 1, 0.0f, nullptr,
-                              BAPS_MODE_E2E_HIF8, stream);
+        return attention_impl(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, knobs_of(nullptr), stream);
     } catch (...) {
         return BAPS_HIP_ERROR;
     }
@@ -291,8 +323,7 @@ int baps_attention_fwd_ex(const void* q, const void* k, const void* v, float* o,
 {
     if (!prm) return BAPS_INVALID_ARGUMENT;
     try {
-        return attention_impl(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, prm->lambda, prm->n_b0,
-                              prm->scale_log2, prm->restart_counts, prm->mode, stream);
+        return attention_impl(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, *prm, stream);
     } catch (...) {
         return BAPS_HIP_ERROR;
     }

@@ -148,6 +148,18 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void baps_attn_decode_kernel(AttnP
     const int r = row_ok ? f / G : 0;
     const int h = g * G + (row_ok ? f % G : 0);
     const int kmax = row_ok ? (p.causal ? min(p.Sk - 1, r + off) : p.Sk - 1) : -1;
+    // tile-level restart (restart_rows > 1, then restart_rows * G <= 16): the
+    // rows c16 == h_local (mod G) of an aligned span of restart_rows * G rows
+    // of the 16 share each block's decision; a ballot takes it
+    const bool tiled = p.restart_rows > 1;
+    uint32_t tmask = 0;
+    if (tiled) {
+        const int RG = p.restart_rows * G;
+        uint32_t pat = 0;
+        for (int j = 0; j < kRows; j += G) pat |= 1u << j;
+        tmask = (pat << (c16 % G)) & (((1u << RG) - 1u) << (RG * (c16 / RG)));
+    }
+    const bool trep = !tiled || c16 == __builtin_ctz(tmask | 0x10000u);   // this lane counts its tile
     int kmax_lo = row_ok ? kmax : 0x7fffffff;
 #pragma unroll
     for (int o = 1; o < 16; o <<= 1) kmax_lo = min(kmax_lo, __shfl_xor(kmax_lo, o, 64));
@@ -237,17 +249,26 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void baps_attn_decode_kernel(AttnP
 
         float nref;
         if constexpr (MODE == kModeE2E) {
-            // block-aware precision rescaling (Alg. 1), per row (see the prefill kernel)
-            const bool vis = amax != ninf;
-            const bool forced = (jb < p.n_b0) || (m == ninf);
+            // block-aware precision rescaling (Alg. 1), per row or per tile (see
+            // the prefill kernel)
+            const bool vis = row_ok && amax != ninf;
+            const bool in_b0 = (jb < p.n_b0) || (p.b0_last && jb == kmax / BLK);
+            const bool forced = in_b0 || (m == ninf);
             const float tq = hif8::round(__builtin_fmaf(amax, c, -m));
-            const bool restart = forced || (ceilf(tq) > lam);
+            bool restart = forced || (ceilf(tq) > lam);
+            bool b1 = vis && !in_b0;
+            if (tiled) {
+                const uint32_t wantb = (uint32_t)__ballot(vis && restart) & tmask;
+                const uint32_t visb = (uint32_t)__ballot(vis) & tmask;
+                const uint32_t b0b = (uint32_t)__ballot(vis && in_b0) & tmask;
+                restart = wantb != 0u;
+                b1 = visb != 0u && b0b == 0u;
+            }
             const float m_hi = __builtin_fmaxf(m, ceilf(amax * c));
             const float m_new = vis ? (restart ? m_hi : m + __builtin_fmaxf(0.0f, ceilf(tq))) : m;
             const float ref_new = vis ? (restart ? m_hi : m) : ref;
-            const bool b1 = vis && (jb >= p.n_b0);
-            n_visit += b1 ? 1u : 0u;
-            n_restart += (b1 && restart) ? 1u : 0u;
+            n_visit += (b1 && trep) ? 1u : 0u;
+            n_restart += (b1 && trep && restart) ? 1u : 0u;
             const float fac = (ref == ninf) ? 1.0f : exp2_int(ref - ref_new);
             if (__any(fac != 1.0f)) {
     #pragma unroll
@@ -374,9 +395,18 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void baps_attn_decode_kernel(AttnP
     if (grp == 0) {
         const float dbias = (CT && MODE != kModeDefault) ? (float)kCodeBiasLog2 : 0.0f;
         if (p.lse) p.lse[((long long)b * p.Hq + h) * p.Sq + r] = empty ? ninf : 0.69314718055994531f * (ref + (log2f(dw) + dbias));
-        if (p.counters && n_visit) {
-            atomicAdd(p.counters + 2 * ((long long)b * p.Hq + h) + 0, (unsigned long long)n_restart);
-            atomicAdd(p.counters + 2 * ((long long)b * p.Hq + h) + 1, (unsigned long long)n_visit);
+        if (n_visit) {
+            if (p.counters) {
+                atomicAdd(p.counters + 2 * ((long long)b * p.Hq + h) + 0, (unsigned long long)n_restart);
+                atomicAdd(p.counters + 2 * ((long long)b * p.Hq + h) + 1, (unsigned long long)n_visit);
+            }
+            if (p.tile_counts) {
+                const int R = p.restart_rows;
+                unsigned long long* tc =
+                    p.tile_counts + 2 * (((long long)b * p.Hq + h) * ((p.Sq + R - 1) / R) + r / R);
+                atomicAdd(tc + 0, (unsigned long long)n_restart);
+                atomicAdd(tc + 1, (unsigned long long)n_visit);
+            }
         }
     }
 }

@@ -124,10 +124,11 @@ __device__ __forceinline__ void load_tile(const uint16_t* base, int key0, int Sk
     }
 }
 
-template <int D, int BLK, int NW, bool CT, int MODE>
+template <int D, int BLK, int NW, bool CT, int MODE, bool TILE>
 __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
 {
     static_assert(MODE == kModeE2E || CT, "the eq. (2) setups use the compact table (T <= 0)");
+    static_assert(MODE == kModeE2E || !TILE, "tile-level restart belongs to Alg. 1");
     static_assert(D == 64 || D == 128, "head dimension");
     static_assert(BLK % 32 == 0 && BLK <= 128, "key block");
     using C = Cfg<D, BLK, NW>;
@@ -135,6 +136,7 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
     // bf16 half of the full score table
     __shared__ __attribute__((aligned(16))) uint8_t ctab[CT ? kCodeHi + 1 : 1];
     __shared__ __attribute__((aligned(16))) uint16_t tab[CT ? 1 : kTabEntries];
+    __shared__ uint32_t tflag[TILE ? NW : 1][3];  // per wave: rows that restart, see the block, are in B0
     extern __shared__ __attribute__((aligned(1024))) char tiles[];
     const uint32_t tiles_lds = (uint32_t)(uintptr_t)LDS_PTR(char, tiles);
 
@@ -212,6 +214,33 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
     kmax_wave_hi = __builtin_amdgcn_readfirstlane(kmax_wave_hi);
     kmax_wave_lo = __builtin_amdgcn_readfirstlane(kmax_wave_lo);
 
+    // Tile-level restart (the paper's granularity, Sec. 3.2): the rows of one
+    // head at restart_rows consecutive query positions share each block's
+    // decision.  With G and R powers of two and R*G <= 256 a tile is the
+    // rows j32 == h_local (mod G) of an aligned span of R*G flattened rows:
+    // inside one wave when R*G <= 32 (a ballot decides), else across
+    // R*G/32 consecutive waves (per-wave masks meet in LDS).
+    // tmask: this lane's tile within the wave's 32 rows (all rows of its
+    // head when the tile spans waves tw0 .. tw0 + twn - 1)
+    uint32_t tmask = 0;
+    int tw0 = 0, twn = 1;
+    bool xwave = false, trep = false;             // trep: this lane counts its tile's blocks
+    if constexpr (TILE) {
+        const int RG = p.restart_rows * G;
+        uint32_t pat = 0;
+        for (int j = 0; j < 32; j += G) pat |= 1u << j;
+        tmask = pat << (j32 % G);
+        xwave = RG > 32;
+        if (!xwave) {
+            tmask &= (RG == 32 ? 0xffffffffu : ((1u << RG) - 1u) << (RG * (j32 / RG)));
+            trep = half == 0 && j32 == __builtin_ctz(tmask);
+        } else {
+            twn = RG / 32;
+            tw0 = wave - wave % twn;
+            trep = half == 0 && wave == tw0 && j32 < G;
+        }
+    }
+
     // Q^T as the B operand of S^T = K Q^T: lane holds Q[row][16*kk + 8*half .. +8]
     u32x4 qop[kDK];
     {
@@ -272,7 +301,15 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
             load_tile<D, BLK, NW, false>(kbase, key0 + BLK, p.Sk, nk, wave, lane);
             load_tile<D, BLK, NW, true>(vbase, key0 + BLK, p.Sk, nk + C::kTileBytes, wave, lane);
         }
-        if (key0 > kmax_wave_hi) continue;                  // nothing visible for this wave
+        if (key0 > kmax_wave_hi) {                          // nothing visible for this wave
+            if constexpr (TILE) {
+                if (xwave) {                                // it still takes part in the tile exchange
+                    if (lane == 0) tflag[wave][0] = tflag[wave][1] = tflag[wave][2] = 0u;
+                    __syncthreads();
+                }
+            }
+            continue;
+        }
 
         // S^T = K_j Q^T.  The wave raises its priority for the MFMA burst so
         // that the two waves sharing a SIMD drift apart: one runs its QK^T
@@ -322,16 +359,51 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
             // path; B1 blocks restart when ceil(rowmax T) > lambda, where rowmax of
             // the 8-bit T = fl32(acc*c - m) is the 8-bit cast of the raw maximum's
             // T (the cast is monotone).
-            const bool vis = amax != ninf;
-            const bool forced = (jb < p.n_b0) || (m == ninf);
+            const bool vis = (!TILE || row_ok) && amax != ninf;
+            const bool in_b0 = (jb < p.n_b0) || (p.b0_last && jb == kmax / BLK);
+            const bool forced = in_b0 || (m == ninf);
             const float tq = hif8::round(__builtin_fmaf(amax, c, -m));
-            const bool restart = forced || (ceilf(tq) > lam);
+            bool restart = forced || (ceilf(tq) > lam);
+            if constexpr (TILE) {
+                // the tile restarts when any of its rows that see the block would
+                const uint32_t wantb = (uint32_t)__ballot(vis && restart);
+                const uint32_t visb = (uint32_t)__ballot(vis);
+                const uint32_t b0b = (uint32_t)__ballot(vis && in_b0);
+                uint32_t tw, tv, tb;
+                if (!xwave) {
+                    tw = wantb & tmask;
+                    tv = visb & tmask;
+                    tb = b0b & tmask;
+                } else {
+                    if (lane == 0) {
+                        tflag[wave][0] = wantb;
+                        tflag[wave][1] = visb;
+                        tflag[wave][2] = b0b;
+                    }
+                    __syncthreads();
+                    uint32_t a = 0, vv = 0, z = 0;
+                    for (int w = tw0; w < tw0 + twn; ++w) {
+                        a |= tflag[w][0];
+                        vv |= tflag[w][1];
+                        z |= tflag[w][2];
+                    }
+                    tw = a & tmask;
+                    tv = vv & tmask;
+                    tb = z & tmask;
+                }
+                restart = tw != 0u;
+                if (trep && tv && !tb) {                    // a B1 tile-block
+                    ++n_visit;
+                    n_restart += restart ? 1u : 0u;
+                }
+            } else {
+                const bool b1 = vis && !in_b0;
+                n_visit += b1 ? 1u : 0u;
+                n_restart += (b1 && restart) ? 1u : 0u;
+            }
             const float m_hi = __builtin_fmaxf(m, ceilf(amax * c));    // ceil(rowmax S), S in fp32
             const float m_new = vis ? (restart ? m_hi : m + __builtin_fmaxf(0.0f, ceilf(tq))) : m;
             const float ref_new = vis ? (restart ? m_hi : m) : ref;
-            const bool b1 = vis && (jb >= p.n_b0);
-            n_visit += b1 ? 1u : 0u;
-            n_restart += (b1 && restart) ? 1u : 0u;
             const float f = (ref == ninf) ? 1.0f : exp2_int(ref - ref_new);
             if (__any(f != 1.0f)) {
     #pragma unroll
@@ -448,38 +520,56 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
         }
     if (half == 0) {
         if (p.lse) p.lse[((long long)b * p.Hq + h) * p.Sq + r] = empty ? ninf : 0.69314718055994531f * (ref + (log2f(d) + dbias));
-        if (p.counters && n_visit) {
-            atomicAdd(p.counters + 2 * ((long long)b * p.Hq + h) + 0, (unsigned long long)n_restart);
-            atomicAdd(p.counters + 2 * ((long long)b * p.Hq + h) + 1, (unsigned long long)n_visit);
+        if ((TILE ? trep : true) && n_visit) {
+            if (p.counters) {
+                atomicAdd(p.counters + 2 * ((long long)b * p.Hq + h) + 0, (unsigned long long)n_restart);
+                atomicAdd(p.counters + 2 * ((long long)b * p.Hq + h) + 1, (unsigned long long)n_visit);
+            }
+            if (p.tile_counts) {
+                const int R = p.restart_rows;
+                unsigned long long* tc =
+                    p.tile_counts + 2 * (((long long)b * p.Hq + h) * ((p.Sq + R - 1) / R) + r / R);
+                atomicAdd(tc + 0, (unsigned long long)n_restart);
+                atomicAdd(tc + 1, (unsigned long long)n_visit);
+            }
         }
     }
 }
 
-template <int D, int BLK, int NW, bool CT, int MODE>
+template <int D, int BLK, int NW, bool CT, int MODE, bool TILE = false>
 hipError_t launch_one(const AttnParams& p, hipStream_t st)
 {
     using C = Cfg<D, BLK, NW>;
     static bool attr_set = false;
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&baps_attn_fwd_kernel<D, BLK, NW, CT, MODE>),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, C::kLdsBytes);
+        hipError_t e = hipFuncSetAttribute(
+            reinterpret_cast<const void*>(&baps_attn_fwd_kernel<D, BLK, NW, CT, MODE, TILE>),
+            hipFuncAttributeMaxDynamicSharedMemorySize, C::kLdsBytes);
         if (e != hipSuccess) return e;
         attr_set = true;
     }
     const long long flat = (long long)p.Sq * (p.Hq / p.Hkv);
     const dim3 grid((unsigned)((flat + C::kTileRows - 1) / C::kTileRows), (unsigned)p.Hkv, (unsigned)p.B);
-    hipLaunchKernelGGL((baps_attn_fwd_kernel<D, BLK, NW, CT, MODE>), grid, dim3(C::kThreads), C::kLdsBytes, st, p);
+    hipLaunchKernelGGL((baps_attn_fwd_kernel<D, BLK, NW, CT, MODE, TILE>), grid, dim3(C::kThreads), C::kLdsBytes,
+                       st, p);
     return hipGetLastError();
 }
 
 template <int D, int BLK>
 hipError_t launch_d_blk(const AttnParams& p, hipStream_t st)
 {
-    // few rows per key/value head (decode, short queries): the HBM-streaming kernel
-    const long long flat = (long long)p.Sq * (p.Hq / p.Hkv);
-    if (flat <= 64) return launch_attention_decode(p, D, BLK, st);
+    // few rows per key/value head (decode, short queries): the HBM-streaming
+    // kernel, which holds a tile of restart_rows query positions when it fits
+    // in its 16 rows
+    const int G = p.Hq / p.Hkv;
+    const long long flat = (long long)p.Sq * G;
+    if (flat <= 64 && (long long)p.restart_rows * G <= 16) return launch_attention_decode(p, D, BLK, st);
     if (p.mode == kModeDefault) return launch_one<D, BLK, 8, true, kModeDefault>(p, st);
     if (p.mode == kModeExp2) return launch_one<D, BLK, 8, true, kModeExp2>(p, st);
+    if (p.restart_rows > 1) {
+        if (p.lambda <= kCodeMaxLambda) return launch_one<D, BLK, 8, true, kModeE2E, true>(p, st);
+        return launch_one<D, BLK, 8, false, kModeE2E, true>(p, st);
+    }
     if (p.lambda <= kCodeMaxLambda) return launch_one<D, BLK, 8, true, kModeE2E>(p, st);
     return launch_one<D, BLK, 8, false, kModeE2E>(p, st);
 }

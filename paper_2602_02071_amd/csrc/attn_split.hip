@@ -315,6 +315,7 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void split_pv_kernel(SplitParams s
     for (int pass = 0; pass < npass; ++pass) {
         const int srow = pass * KW + wave;
         const bool row_ok = srow < nr;
+        const int last_blk = row_ok ? row_info(p, tile, g, srow).kmax / BLK : -1;   // B0 with b0_last
         float m = ninf;
         unsigned n_restart = 0, n_visit = 0;
         if (pass > 0) {                           // this pass's first windows (the V ring is already in flight)
@@ -333,7 +334,7 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void split_pv_kernel(SplitParams s
                 if (!(row_ok && jb < j1)) amax = ninf;
                 const bool vis = amax != ninf;
                 const float ceil_ac = ceilf(amax * c);
-                const bool in_b0 = jb < p.n_b0;
+                const bool in_b0 = jb < p.n_b0 || (p.b0_last && jb == last_blk);
                 const bool mine = row_ok && jb >= j0 && jb < j1;
                 int lo = 0;
                 for (;;) {
@@ -348,7 +349,7 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void split_pv_kernel(SplitParams s
                     const int f = bal ? (int)__builtin_ctzll(bal) : 64;
                     if (pend && lane <= f && mine) {
                         refs_l[srow * kSplitMaxBps + (jb - j0)] = ref_new;   // -inf: no visible key
-                        const bool b1 = vis && jb >= p.n_b0;
+                        const bool b1 = vis && !in_b0;
                         n_visit += b1 ? 1u : 0u;
                         n_restart += (b1 && restart) ? 1u : 0u;
                     }
@@ -475,13 +476,20 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void split_pv_kernel(SplitParams s
             prow[D + 1] = cur;
         }
     }
-    // restart counters of this split's blocks
-    if (p.counters && tid < kRows) {
+    // restart counters of this split's blocks (a tile is one row here)
+    if (tid < kRows) {
         const RowInfo cr = row_info(p, tile, g, tid);
         if (cr.ok && s_cnt[tid][1]) {
-            unsigned long long* cp = p.counters + 2 * ((long long)b * p.Hq + cr.h);
-            atomicAdd(cp + 0, (unsigned long long)s_cnt[tid][0]);
-            atomicAdd(cp + 1, (unsigned long long)s_cnt[tid][1]);
+            if (p.counters) {
+                unsigned long long* cp = p.counters + 2 * ((long long)b * p.Hq + cr.h);
+                atomicAdd(cp + 0, (unsigned long long)s_cnt[tid][0]);
+                atomicAdd(cp + 1, (unsigned long long)s_cnt[tid][1]);
+            }
+            if (p.tile_counts) {
+                unsigned long long* tc = p.tile_counts + 2 * (((long long)b * p.Hq + cr.h) * p.Sq + cr.r);
+                atomicAdd(tc + 0, (unsigned long long)s_cnt[tid][0]);
+                atomicAdd(tc + 1, (unsigned long long)s_cnt[tid][1]);
+            }
         }
     }
 }

@@ -54,10 +54,13 @@ struct AttnParams {
     float* lse;                 // [B, Hq, Sq] or null
     const uint32_t* tab;        // score table (device)
     const uint8_t* ctab;        // compact code table (device), kCodeTableBytes bytes (entries, then zeros)
-    unsigned long long* counters;  // [B*Hq][2] restarted / visited B1 row-blocks, or null
+    unsigned long long* counters;  // [B*Hq][2] restarted / visited B1 tile-blocks, or null
+    unsigned long long* tile_counts;  // [B*Hq][ceil(Sq/R)][2] the same per tile, or null
     int B, Hq, Hkv, Sq, Sk;
     int causal, lambda, n_b0;
     int mode;                   // kModeE2E, kModeDefault or kModeExp2
+    int restart_rows;           // R: query positions of one head sharing the restart decision
+    int b0_last;                // B0 also holds each row's last visible key block
     float c;                    // log2(e)/sqrt(D) as fp32 (or the caller's override)
 };
 

@@ -77,6 +77,23 @@ def test_attention_argument_checks(lib):
     assert lib.baps_attention_fwd_ex(16, 16, 16, 16, None, 1, 1, 1, 4, 4, 64, 0, 64, None, None) == 1
 
 
+def test_tile_restart_argument_checks(lib):
+    """Tile-level restart needs powers of two that keep a tile inside one
+    workgroup (no GPU work: the checks run before any HIP call)."""
+    def ex(Hq, Hkv, Sq, R, mode=0):
+        prm = baps.baps_params_t(1, 1, 0.0, None, mode, R, 0, None)
+        return lib.baps_attention_fwd_ex(16, 16, 16, 16, None, 1, Hq, Hkv, Sq, 64, 64, 1, 64, ctypes.byref(prm), None)
+    assert ex(8, 2, 64, -1) == 1                 # negative tile height
+    assert ex(8, 2, 64, 3) == 2                  # not a power of two
+    assert ex(6, 2, 64, 2) == 2                  # Hq/Hkv = 3: not a power of two
+    assert ex(32, 1, 64, 16) == 2                # 16 positions x 32 heads > 256 rows
+    assert ex(8, 2, 64, 2, mode=baps.BAPS_MODE_DEFAULT) == 2   # eq. (2) setups have no restarts
+    assert ex(8, 2, 0, 3) == 0                   # empty work is checked first
+    assert baps.baps_attention_split_workspace(1, 32, 8, 4, 32768, 128, 128, restart_rows=4) == 0
+    assert baps.baps_attention_split_workspace(1, 32, 8, 1, 32768, 128, 128, restart_rows=4) > 0   # Sq = 1
+    assert baps.baps_attention_split_workspace(1, 32, 8, 1, 32768, 128, 128, b0_last=True) > 0
+
+
 def test_split_workspace_and_checks(lib):
     P = ctypes.POINTER(baps.baps_params_t)
     # the split path is taken for few streams and many keys only
