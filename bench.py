@@ -134,6 +134,50 @@ def softmax_setups(cfg, steps=20):
     return res
 
 
+def restart_rates(cfgs=(2, 4, 3), lams=(0, 1, 2), tile_rows=64, steps=10):
+    """The synthetic analogue of the paper's restart-rate table (Sec. 4.3,
+    Table 4): per workload and lambda, the average restart rate (ARR:
+    restarted over visited B1 tile-blocks) and the peak restart rate (PRR:
+    the largest rate of any one tile's output), from the kernels' per-tile
+    counters.  Tiles are tile_rows query positions of one head (one row at
+    Sq = 1); B0 is the first block and each row's diagonal block.  Also the
+    time of the tiled pass against the canonical per-row pass (lambda 1)."""
+    import torch
+    import paper_2602_02071_amd as baps
+    from paper_2602_02071_amd.workloads import make_workload
+    dev = torch.device("cuda:0")
+    out = {}
+    for cfg in cfgs:
+        w, q, k, v = make_workload(cfg)
+        qt, kt, vt = (torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).to(dev) for x in (q, k, v))
+        o = torch.empty((w.B, w.Hq, w.Sq, w.D), dtype=torch.float32, device=dev)
+        lse = torch.empty((w.B, w.Hq, w.Sq), dtype=torch.float32, device=dev)
+        stream = torch.cuda.current_stream().cuda_stream
+        R = tile_rows if w.Sq > 1 else 1
+        ntq = (w.Sq + R - 1) // R
+        rec = {"workload": w.name, "restart_rows": R, "b0": "first and diagonal block"}
+        for lam in lams:
+            tc = torch.zeros((w.B * w.Hq * ntq, 2), dtype=torch.int64, device=dev)
+            baps.baps_attention_fwd_ex(qt, kt, vt, o, lse, w.B, w.Hq, w.Hkv, w.Sq, w.Sk, w.D, w.causal, w.block,
+                                       lam=lam, stream=stream, restart_rows=R, b0_last=True, tile_counts=tc)
+            torch.cuda.synchronize()
+            c = tc.cpu().numpy().astype(np.float64)
+            seen = c[:, 1] > 0
+            rec[f"lambda_{lam}"] = {"ARR": float(c[:, 0].sum() / max(c[:, 1].sum(), 1.0)),
+                                    "PRR": float((c[seen, 0] / c[seen, 1]).max()) if seen.any() else 0.0,
+                                    "tiles": int(seen.sum())}
+        times = {}
+        for name, rr in (("per_row", 1), ("tiled", R)):
+            def step():
+                baps.baps_attention_fwd_ex(qt, kt, vt, o, lse, w.B, w.Hq, w.Hkv, w.Sq, w.Sk, w.D, w.causal,
+                                           w.block, stream=stream, restart_rows=rr, b0_last=rr > 1)
+            _, per = _time_launches(step, steps, 2, 30.0)
+            times[name] = float(np.mean(per)) * 1e3
+        rec["us"] = times
+        out[f"workload_{cfg}"] = rec
+    return out
+
+
 def single_sequence_decode(steps=20):
     """One sequence, long context (B=1, Hq=32, Hkv=8, Sq=1, Sk=32768, D=128,
     block 128): the one-pass decode kernel (8 streams) against the split-key
@@ -237,6 +281,7 @@ def main():
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-boundary", action="store_true", help="skip the codec / softmax-block kernels")
     ap.add_argument("--no-modes", action="store_true", help="skip the Default / Exp2 HiF8 comparison")
+    ap.add_argument("--no-restart-rates", action="store_true", help="skip the tile restart-rate table")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -282,6 +327,8 @@ def main():
                                       "frac": gbs / PEAK_HBM_GBS, "traffic": _traffic("attn_fwd_decode")}}
     if not args.no_modes and w.Sq > 1:
         out["softmax_setups"] = softmax_setups(args.config)
+    if not args.no_restart_rates:
+        out["restart_rates"] = restart_rates()
     if not args.no_decode and args.config != 3:
         out["decode_single_sequence"] = single_sequence_decode()
     if not args.no_boundary:
