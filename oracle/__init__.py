@@ -14,6 +14,7 @@ library in ``paper_2602_02071_amd``, and that library never imports it.
 from __future__ import annotations
 
 import ctypes
+import math
 import os
 import subprocess
 
@@ -86,11 +87,11 @@ def _load():
                                 i32, i32, i32, i32, d, P, i64, P, P, P, i32]
     L.orc_attention_ex.restype = i32
     L.orc_attention_ex.argtypes = [P, P, P, i32, i32, i32, i32, i32, i32, i32, i32,
-                                   i32, i32, i32, i32, d, P, i64, P, P, P, P, d, ctypes.c_uint64, i32, i32]
+                                   i32, i32, i32, i32, d, P, i64, P, P, P, P, d, ctypes.c_uint64, i32, i32, i32]
     L.orc_attention_tiles.restype = i32
     L.orc_attention_tiles.argtypes = [P, P, P, i32, i32, i32, i32, i32, i32, i32, i32,
                                       i32, i32, i32, i32, i32, i32, d, P, i64, P, P, P, P, P, d,
-                                      ctypes.c_uint64, i32]
+                                      ctypes.c_uint64, i32, i32]
     L.orc_exact_attention.restype = i32
     L.orc_exact_attention.argtypes = [P, P, P, i32, i32, i32, i32, i32, i32, i32,
                                       d, P, i64, P, P, i32]
@@ -193,7 +194,7 @@ def _rows(rows, total):
 
 def attention(q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, block, mode=E2E_HIF8, lam=1, n_b0=1,
               literal_else=False, scale_log2=0.0, rows=None, nthreads=0, margin=False, jitter=0.0,
-              jitter_seed=0, pv_bf16=False, restart_rows=1, b0_last=False, visits=False):
+              jitter_seed=0, pv_bf16=False, restart_rows=1, b0_last=False, visits=False, qk_fp8=False):
     """Attention rows in one of the paper's setups.
 
     q: [B,Hq,Sq,D], k/v: [B,Hkv,Sk,D] bf16 bit patterns.  rows: global row
@@ -213,7 +214,10 @@ def attention(q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, block, mode=E2E_HIF8, lam=
     positions of one head, B0 also holds each row's last key block when
     b0_last, and the counts are per tile: restarts[n] (and, with visits,
     one more array of visited B1 tile-blocks before the margin) hold the
-    row's tile's restarted B1 tile-blocks."""
+    row's tile's restarted B1 tile-blocks.
+
+    qk_fp8: q and k carry FP8 E4M3 values (as bf16 patterns, e4m3_to_bf16):
+    the margins and jitters use the FP8 matrix unit's accumulation bound."""
     L = _load()
     q, k, v = _bits(q), _bits(k), _bits(v)
     rows = _rows(rows, B * Hq * Sq)
@@ -228,7 +232,7 @@ def attention(q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, block, mode=E2E_HIF8, lam=
                                    int(mode), int(lam), int(n_b0), int(bool(b0_last)), int(restart_rows),
                                    int(literal_else), float(scale_log2), _ptr(rows), n, _ptr(o), _ptr(lse),
                                    _ptr(nrs), _ptr(nvs), _ptr(mg), float(jitter),
-                                   ctypes.c_uint64(int(jitter_seed)), int(nthreads))
+                                   ctypes.c_uint64(int(jitter_seed)), int(nthreads), int(bool(qk_fp8)))
         if st:
             raise ValueError("oracle rejected the attention arguments")
         out = (o, lse, nrs) + ((nvs,) if visits else ()) + ((mg,) if margin else ())
@@ -236,12 +240,37 @@ def attention(q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, block, mode=E2E_HIF8, lam=
     st = L.orc_attention_ex(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, Sq, Sk, D, int(causal), block,
                             int(mode), int(lam), int(n_b0), int(literal_else), float(scale_log2),
                             _ptr(rows), n, _ptr(o), _ptr(lse), _ptr(nrs), _ptr(mg), float(jitter),
-                            ctypes.c_uint64(int(jitter_seed)), int(nthreads), int(bool(pv_bf16)))
+                            ctypes.c_uint64(int(jitter_seed)), int(nthreads), int(bool(pv_bf16)),
+                            int(bool(qk_fp8)))
     if st:
         raise ValueError("oracle rejected the attention arguments")
     if margin:
         return o, lse, nrs, mg
     return o, lse, nrs
+
+
+def e4m3_to_bf16(codes) -> np.ndarray:
+    """FP8 E4M3 (OCP) codes -> bf16 bit patterns of the same values, exactly:
+    every finite E4M3 value (3 mantissa bits, exponents -9 .. 8) is a bf16
+    value.  NaN codes (0x7F, 0xFF) are rejected."""
+    L = _load()
+    c = np.ascontiguousarray(codes, dtype=np.uint8)
+    table = np.array([L.orc_e4m3_decode(i) for i in range(256)], dtype=np.float64)
+    if np.isnan(table[c]).any():
+        raise ValueError("NaN FP8 code in q or k")
+    f32 = table.astype(np.float32)
+    bits = (f32.view(np.uint32) >> 16).astype(np.uint16)
+    assert np.array_equal((bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)[~np.isnan(table)],
+                          table[~np.isnan(table)])
+    return bits[c]
+
+
+def fp8_scale_log2(D, q_scale, k_scale, scale_log2=0.0) -> float:
+    """The score scale with FP8 Q/K: c' = c * q_scale * k_scale in double
+    (the scales as fp32), rounded once to fp32 by the attention path; c is
+    scale_log2 or log2(e)/sqrt(D)."""
+    base = float(scale_log2) if scale_log2 else math.log2(math.e) / math.sqrt(D)
+    return base * float(np.float32(q_scale)) * float(np.float32(k_scale))
 
 
 def exact_attention(q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, scale_log2=0.0, rows=None, nthreads=0):

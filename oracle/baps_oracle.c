@@ -367,6 +367,7 @@ typedef struct {
     double jitter;          /* move each dot product by jitter * its error bound */
     uint64_t jitter_seed;   /* 0: every dot product moves the same way; else random signs */
     int pv_bf16;            /* eq. (2) setups: P enters the P V product rounded to bf16 */
+    int qk_fp8;             /* q and k carry FP8 E4M3 values: the FP8 matrix unit's error bound */
 } attn_job;
 
 static inline double bf16_to_double(uint16_t b)
@@ -402,6 +403,31 @@ static double abs_dot64(const uint16_t* a, const uint16_t* b, int D)
     double s = 0.0;
     for (int i = 0; i < D; ++i) s += fabs(bf16_to_double(a[i]) * bf16_to_double(b[i]));
     return s;
+}
+
+/* The error bound of the matrix unit's dot product, in the units of acc.
+ * bf16 operands: fp32 accumulation, ACC_ERR * 2^-24 * sum |q_d k_d|.  FP8
+ * operands (the gfx950 FP8 matrix instructions): each step of 64 values of d
+ * is summed with about 12 bits below its largest product (measured up to
+ * 5700 units of 2^-24 * (largest |q_d k_d| of each step + |q.k|) over
+ * normal and outlier-channel data, for both the 32x32x64 and the 16x16x128
+ * forms); the bound is 2^-10 times that, plus the fp32 term. */
+static double acc_err(const attn_job* J, const uint16_t* a, const uint16_t* b, int D)
+{
+    double e = ACC_ERR * ldexp(abs_dot64(a, b, D), -24);
+    if (J->qk_fp8) {
+        double gm = 0.0;
+        for (int g0 = 0; g0 < D; g0 += 64) {
+            double mx = 0.0;
+            for (int i = g0; i < g0 + 64 && i < D; ++i) {
+                const double p = fabs(bf16_to_double(a[i]) * bf16_to_double(b[i]));
+                if (p > mx) mx = p;
+            }
+            gm += mx;
+        }
+        e += ldexp(gm + fabs(dot64(a, b, D)), -10);
+    }
+    return e;
 }
 
 static uint64_t splitmix64(uint64_t x)
@@ -468,7 +494,7 @@ static void row_alg1(const attn_job* J, int b, int h, int r, row_scratch* W,
     for (int c = 0; c <= kmax; ++c) {
         const uint16_t* kr = kb + (int64_t)c * D;
         double a = dot64(qr, kr, D);
-        const double e_acc = ACC_ERR * ldexp(abs_dot64(qr, kr, D), -24);
+        const double e_acc = acc_err(J, qr, kr, D);
         if (J->jitter != 0.0) {
             double sgn = 1.0;
             if (J->jitter_seed) sgn = (splitmix64(J->jitter_seed ^ (rowid * 1000003ull + (uint64_t)c)) & 1) ? 1.0 : -1.0;
@@ -626,7 +652,7 @@ static void row_eq2(const attn_job* J, int b, int h, int r, row_scratch* W, doub
         for (int c = 0; c < nc; ++c) {
             const uint16_t* kr = kb + (int64_t)(c0 + c) * D;
             double a = dot64(qr, kr, D);
-            const double e_acc = ACC_ERR * ldexp(abs_dot64(qr, kr, D), -24);
+            const double e_acc = acc_err(J, qr, kr, D);
             if (J->jitter != 0.0) {
                 double sgn = 1.0;
                 if (J->jitter_seed)
@@ -782,11 +808,11 @@ int orc_attention_ex(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                      int B, int Hq, int Hkv, int Sq, int Sk, int D, int causal, int block,
                      int mode, int lambda, int n_b0, int literal_else, double scale_log2,
                      const int64_t* rows, int64_t nrows, double* o, double* lse, int32_t* nrestart,
-                     double* margin, double jitter, uint64_t jitter_seed, int nthreads, int pv_bf16)
+                     double* margin, double jitter, uint64_t jitter_seed, int nthreads, int pv_bf16, int qk_fp8)
 {
     if (attn_check(B, Hq, Hkv, Sq, Sk, D, block) || mode < 0 || mode > 7) return 1;
     attn_job J = { q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, block, mode, lambda, n_b0,
-                   literal_else, 0.0f, 0.0, rows, o, lse, nrestart, margin, jitter, jitter_seed, pv_bf16 };
+                   literal_else, 0.0f, 0.0, rows, o, lse, nrestart, margin, jitter, jitter_seed, pv_bf16, qk_fp8 };
     J.c64 = scale_log2 != 0.0 ? scale_log2 : M_LOG2E / sqrt((double)D);
     J.c32 = (float)J.c64;
     if (mode != ORC_E2E_EXACT) J.c64 = (double)J.c32;
@@ -803,7 +829,7 @@ int orc_attention(const uint16_t* q, const uint16_t* k, const uint16_t* v,
 {
     return orc_attention_ex(q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, block, mode, lambda, n_b0,
                             literal_else, scale_log2, rows, nrows, o, lse, nrestart, NULL, 0.0, 0,
-                            nthreads, 0);
+                            nthreads, 0, 0);
 }
 
 /* ------------------------------------------------------------------------ */
@@ -855,7 +881,7 @@ static void tile_alg1(const attn_job* J, int b0_last, int b, int h, int r0, int 
         for (int c = 0; c <= T->kmax[i]; ++c) {                          /* as in row_alg1 */
             const uint16_t* kr = kb + (int64_t)c * D;
             double a = dot64(qr, kr, D);
-            const double e_acc = ACC_ERR * ldexp(abs_dot64(qr, kr, D), -24);
+            const double e_acc = acc_err(J, qr, kr, D);
             if (J->jitter != 0.0) {
                 double sgn = 1.0;
                 if (J->jitter_seed)
@@ -1050,12 +1076,12 @@ int orc_attention_tiles(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                         int mode, int lambda, int n_b0, int b0_last, int restart_rows, int literal_else,
                         double scale_log2, const int64_t* rows, int64_t nrows, double* o, double* lse,
                         int32_t* nrestart, int32_t* nvisit, double* margin, double jitter,
-                        uint64_t jitter_seed, int nthreads)
+                        uint64_t jitter_seed, int nthreads, int qk_fp8)
 {
     if (attn_check(B, Hq, Hkv, Sq, Sk, D, block)) return 1;
     if ((mode != ORC_E2E_HIF8 && mode != ORC_E2E_EXACT) || restart_rows < 1 || n_b0 < 0) return 1;
     attn_job J = { q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, block, mode, lambda, n_b0,
-                   literal_else, 0.0f, 0.0, rows, o, lse, nrestart, margin, jitter, jitter_seed, 0 };
+                   literal_else, 0.0f, 0.0, rows, o, lse, nrestart, margin, jitter, jitter_seed, 0, qk_fp8 };
     J.c64 = scale_log2 != 0.0 ? scale_log2 : M_LOG2E / sqrt((double)D);
     J.c32 = (float)J.c64;
     if (mode != ORC_E2E_EXACT) J.c64 = (double)J.c32;

@@ -109,6 +109,36 @@ def make_qkv(B, Hq, Hkv, Sq, Sk, D, seed=0, outliers=False, sink=0, lognormal_k=
     return f32_to_bf16_bits(q), f32_to_bf16_bits(k), f32_to_bf16_bits(v)
 
 
+def quantize_e4m3(x: np.ndarray, scale: float) -> np.ndarray:
+    """OCP FP8 E4M3 codes of x / scale: round to nearest, ties to even,
+    saturating at +-448 (the inputs of the FP8 Q/K path)."""
+    y = np.asarray(x, dtype=np.float64) / float(np.float32(scale))
+    a = np.minimum(np.abs(y), 448.0)
+    e = np.floor(np.log2(np.maximum(a, 2.0 ** -9)))
+    e = np.maximum(e, -6.0)                           # subnormals share the step 2^-9
+    step = 2.0 ** (e - 3)
+    q = np.round(a / step) * step                     # numpy rounds ties to even
+    q = np.minimum(q, 448.0)
+    e2 = np.floor(np.log2(np.maximum(q, 2.0 ** -9)))
+    norm = q >= 2.0 ** -6
+    m_norm = np.round(q / 2.0 ** e2 * 8.0 - 8.0)
+    code = np.where(norm, ((e2 + 7).astype(np.int64) << 3) | m_norm.astype(np.int64),
+                    np.round(q / 2.0 ** -9).astype(np.int64))
+    code = np.where(q == 0, 0, code)
+    return (code | np.where(np.signbit(y) & (q > 0), 0x80, 0)).astype(np.uint8)
+
+
+def make_qk_fp8(q_bits: np.ndarray, k_bits: np.ndarray):
+    """FP8 E4M3 codes of bf16 Q and K with per-tensor power-of-two scales
+    that put each tensor's largest magnitude near the top of the format."""
+    out = []
+    for bits in (q_bits, k_bits):
+        amax = float(np.abs(bf16_bits_to_f32(bits)).max()) or 1.0
+        scale = 2.0 ** np.ceil(np.log2(amax / 448.0))
+        out += [quantize_e4m3(bf16_bits_to_f32(bits), scale), scale]
+    return out[0], out[2], out[1], out[3]
+
+
 def make_workload(cfg: int):
     """(Workload, q, k, v) of one of the five configurations, seed = cfg."""
     w = WORKLOADS[cfg]
