@@ -95,7 +95,19 @@ typedef struct {
     unsigned long long* tile_counts;     /* device [B*Hq][ceil(Sq/restart_rows)][2]: restarted
                                             and visited B1 blocks per tile (Table 4's restart
                                             rates); caller-zeroed, NULL to skip               */
+    int qk_format;                       /* BAPS_QK_BF16 (0) or BAPS_QK_FP8_E4M3 (1): q and k
+                                            hold OCP FP8 E4M3 codes (one byte per element,
+                                            rows of D bytes) for the values
+                                            q_scale * code and k_scale * code; the scales fold
+                                            into the score scale, T = fl32(acc * c' - ref) with
+                                            c' = fl32(c * q_scale * k_scale) (Sec. 3.2: T is
+                                            computed in the dequantisation).  Not with
+                                            restart_rows > 1                                  */
+    float q_scale, k_scale;              /* FP8 dequantisation scales (finite, > 0)            */
 } baps_params_t;
+
+#define BAPS_QK_BF16 0
+#define BAPS_QK_FP8_E4M3 1
 
 /* baps_attention_fwd with explicit knobs; p must not be NULL; scale_log2
  * must be >= 0. */

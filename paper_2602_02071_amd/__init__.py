@@ -36,13 +36,17 @@ class BapsError(RuntimeError):
 class baps_params_t(ctypes.Structure):
     _fields_ = [("lambda_", ctypes.c_int), ("n_b0", ctypes.c_int), ("scale_log2", ctypes.c_float),
                 ("restart_counts", ctypes.c_void_p), ("mode", ctypes.c_int), ("restart_rows", ctypes.c_int),
-                ("b0_last", ctypes.c_int), ("tile_counts", ctypes.c_void_p)]
+                ("b0_last", ctypes.c_int), ("tile_counts", ctypes.c_void_p), ("qk_format", ctypes.c_int),
+                ("q_scale", ctypes.c_float), ("k_scale", ctypes.c_float)]
 
 
 # softmax setups (include/baps.h)
 BAPS_MODE_E2E_HIF8 = 0
 BAPS_MODE_DEFAULT = 1
 BAPS_MODE_EXP2_HIF8 = 2
+# Q/K formats (include/baps.h)
+BAPS_QK_BF16 = 0
+BAPS_QK_FP8_E4M3 = 1
 
 
 def load():
@@ -114,30 +118,33 @@ def baps_attention_fwd(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, st
 
 
 def _params(lam=1, n_b0=1, scale_log2=0.0, restart_counts=None, mode=BAPS_MODE_E2E_HIF8, restart_rows=1,
-            b0_last=False, tile_counts=None):
+            b0_last=False, tile_counts=None, qk_scales=None):
+    fmt, qs, ks = (BAPS_QK_BF16, 1.0, 1.0) if qk_scales is None else (BAPS_QK_FP8_E4M3,) + tuple(qk_scales)
     return baps_params_t(int(lam), int(n_b0), float(scale_log2), _p(restart_counts), int(mode), int(restart_rows),
-                         int(bool(b0_last)), _p(tile_counts))
+                         int(bool(b0_last)), _p(tile_counts), int(fmt), float(qs), float(ks))
 
 
 def baps_attention_fwd_ex(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, lam=1, n_b0=1,
                           scale_log2=0.0, restart_counts=None, stream=None, mode=BAPS_MODE_E2E_HIF8,
-                          restart_rows=1, b0_last=False, tile_counts=None):
-    prm = _params(lam, n_b0, scale_log2, restart_counts, mode, restart_rows, b0_last, tile_counts)
+                          restart_rows=1, b0_last=False, tile_counts=None, qk_scales=None):
+    """qk_scales=(q_scale, k_scale): q and k are FP8 E4M3 codes (uint8 tensors)."""
+    prm = _params(lam, n_b0, scale_log2, restart_counts, mode, restart_rows, b0_last, tile_counts, qk_scales)
     _check("baps_attention_fwd_ex", load().baps_attention_fwd_ex(
         _p(q), _p(k), _p(v), _p(o), _p(lse), B, Hq, Hkv, Sq, Sk, D, int(causal), block,
         ctypes.byref(prm), _stream(stream)))
 
 
 def baps_attention_split_workspace(B, Hq, Hkv, Sq, Sk, D, block, lam=1, n_b0=1, scale_log2=0.0,
-                                   mode=BAPS_MODE_E2E_HIF8, restart_rows=1, b0_last=False):
-    prm = _params(lam, n_b0, scale_log2, None, mode, restart_rows, b0_last)
+                                   mode=BAPS_MODE_E2E_HIF8, restart_rows=1, b0_last=False, qk_scales=None):
+    prm = _params(lam, n_b0, scale_log2, None, mode, restart_rows, b0_last, None, qk_scales)
     return int(load().baps_attention_split_workspace(B, Hq, Hkv, Sq, Sk, D, block, ctypes.byref(prm)))
 
 
 def baps_attention_fwd_split(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, workspace, workspace_bytes,
                              lam=1, n_b0=1, scale_log2=0.0, restart_counts=None, stream=None,
-                             mode=BAPS_MODE_E2E_HIF8, restart_rows=1, b0_last=False, tile_counts=None):
-    prm = _params(lam, n_b0, scale_log2, restart_counts, mode, restart_rows, b0_last, tile_counts)
+                             mode=BAPS_MODE_E2E_HIF8, restart_rows=1, b0_last=False, tile_counts=None,
+                             qk_scales=None):
+    prm = _params(lam, n_b0, scale_log2, restart_counts, mode, restart_rows, b0_last, tile_counts, qk_scales)
     _check("baps_attention_fwd_split", load().baps_attention_fwd_split(
         _p(q), _p(k), _p(v), _p(o), _p(lse), B, Hq, Hkv, Sq, Sk, D, int(causal), block,
         ctypes.byref(prm), _p(workspace), int(workspace_bytes), _stream(stream)))
@@ -170,32 +177,36 @@ def baps_init():
 
 # ------------------------------------------------------------ tensor helpers
 def attention(q, k, v, causal, block, lse=True, lam=None, n_b0=None, scale_log2=0.0, restart_counts=None,
-              stream=None, mode=BAPS_MODE_E2E_HIF8, split=False, restart_rows=1, b0_last=False, tile_counts=None):
+              stream=None, mode=BAPS_MODE_E2E_HIF8, split=False, restart_rows=1, b0_last=False, tile_counts=None,
+              qk_scales=None):
     """Allocate O (and lse) with torch on q's device and run the fused pass.
     q [B,Hq,Sq,D], k/v [B,Hkv,Sk,D] bf16 CUDA tensors, contiguous.  split:
     take baps_attention_fwd_split, with a workspace allocated here.
     restart_rows / b0_last / tile_counts: the tile-level restart knobs of
-    baps_params_t."""
+    baps_params_t.  qk_scales=(q_scale, k_scale): q and k are FP8 E4M3 codes
+    (uint8 tensors) with those dequantisation scales."""
     import torch
     B, Hq, Sq, D = q.shape
     Hkv, Sk = k.shape[1], k.shape[2]
-    for t in (q, k, v):
-        if t.dtype != torch.bfloat16 or not t.is_contiguous() or not t.is_cuda:
-            raise ValueError("q, k, v must be contiguous bf16 device tensors")
+    qk_dtype = torch.bfloat16 if qk_scales is None else torch.uint8
+    for t, dt in ((q, qk_dtype), (k, qk_dtype), (v, torch.bfloat16)):
+        if t.dtype != dt or not t.is_contiguous() or not t.is_cuda:
+            raise ValueError("q, k (bf16, or uint8 FP8 codes with qk_scales) and v (bf16) must be contiguous "
+                             "device tensors")
     o = torch.empty((B, Hq, Sq, D), dtype=torch.float32, device=q.device)
     l = torch.empty((B, Hq, Sq), dtype=torch.float32, device=q.device) if lse else None
+    lam_, nb_ = 1 if lam is None else lam, 1 if n_b0 is None else n_b0
     if split:
-        lam_, nb_ = 1 if lam is None else lam, 1 if n_b0 is None else n_b0
         nbytes = baps_attention_split_workspace(B, Hq, Hkv, Sq, Sk, D, block, lam_, nb_, scale_log2, mode,
-                                                restart_rows, b0_last)
+                                                restart_rows, b0_last, qk_scales)
         ws = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=q.device)
         baps_attention_fwd_split(q, k, v, o, l, B, Hq, Hkv, Sq, Sk, D, causal, block, ws, nbytes, lam_, nb_,
-                                 scale_log2, restart_counts, stream, mode, restart_rows, b0_last, tile_counts)
+                                 scale_log2, restart_counts, stream, mode, restart_rows, b0_last, tile_counts,
+                                 qk_scales)
     elif (lam is None and n_b0 is None and not scale_log2 and restart_counts is None and mode == BAPS_MODE_E2E_HIF8
-          and restart_rows == 1 and not b0_last and tile_counts is None):
+          and restart_rows == 1 and not b0_last and tile_counts is None and qk_scales is None):
         baps_attention_fwd(q, k, v, o, l, B, Hq, Hkv, Sq, Sk, D, causal, block, stream)
     else:
-        baps_attention_fwd_ex(q, k, v, o, l, B, Hq, Hkv, Sq, Sk, D, causal, block,
-                              1 if lam is None else lam, 1 if n_b0 is None else n_b0, scale_log2,
-                              restart_counts, stream, mode, restart_rows, b0_last, tile_counts)
+        baps_attention_fwd_ex(q, k, v, o, l, B, Hq, Hkv, Sq, Sk, D, causal, block, lam_, nb_, scale_log2,
+                              restart_counts, stream, mode, restart_rows, b0_last, tile_counts, qk_scales)
     return o, l

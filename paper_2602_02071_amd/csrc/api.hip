@@ -176,10 +176,14 @@ int make_params(const void* q, const void* k, const void* v, float* o, float* ls
         return BAPS_INVALID_ARGUMENT;
     if (!(D == 64 || D == 128) || !(block == 32 || block == 64 || block == 128)) return BAPS_UNSUPPORTED;
     if ((long long)Sq * (Hq / Hkv) > 0x7fffffffLL || Hkv > 65535 || B > 65535) return BAPS_UNSUPPORTED;
+    if (kn.qk_format != BAPS_QK_BF16 && kn.qk_format != BAPS_QK_FP8_E4M3) return BAPS_INVALID_ARGUMENT;
+    const bool f8 = kn.qk_format == BAPS_QK_FP8_E4M3;
+    if (f8 && !(kn.q_scale > 0.0f && kn.k_scale > 0.0f && std::isfinite(kn.q_scale) && std::isfinite(kn.k_scale)))
+        return BAPS_INVALID_ARGUMENT;
     const int G = Hq / Hkv;
     if (kn.restart_rows > 1 && !pow2(kn.restart_rows)) return BAPS_UNSUPPORTED;
     const int R = effective_rows(kn.restart_rows, Sq);
-    if (R > 1 && (mode != BAPS_MODE_E2E_HIF8 || !pow2(G) || G > 32 || (long long)R * G > 256))
+    if (R > 1 && (mode != BAPS_MODE_E2E_HIF8 || !pow2(G) || G > 32 || (long long)R * G > 256 || f8))
         return BAPS_UNSUPPORTED;
     AttnParams& p = *out;
     p.tab = nullptr;
@@ -198,7 +202,12 @@ int make_params(const void* q, const void* k, const void* v, float* o, float* ls
     p.mode = mode;
     p.restart_rows = R;
     p.b0_last = kn.b0_last ? 1 : 0;
-    p.c = kn.scale_log2 > 0.0f ? kn.scale_log2 : (float)(1.4426950408889634 / std::sqrt((double)D));
+    p.qk_f8 = f8 ? 1 : 0;
+    // the score scale in log2 units; with FP8 Q/K the dequantisation scales
+    // fold into it, in double, rounded once
+    const double base = kn.scale_log2 > 0.0f ? (double)kn.scale_log2 : 1.4426950408889634 / std::sqrt((double)D);
+    p.c = (float)(f8 ? base * (double)kn.q_scale * (double)kn.k_scale : base);
+    if (!(p.c > 0.0f) || std::isinf(p.c)) return BAPS_UNSUPPORTED;
     return BAPS_OK;
 }
 
@@ -242,6 +251,7 @@ SplitPlan split_plan(int B, int Hq, int Hkv, int Sq, int Sk, int D, int block, c
     if (!(D == 64 || D == 128) || !(block == 32 || block == 64 || block == 128)) return sp;
     if (kn.mode != BAPS_MODE_E2E_HIF8 || kn.lambda > kCodeMaxLambda) return sp;
     if (kn.restart_rows < 0 || effective_rows(kn.restart_rows, Sq) > 1) return sp;   // per-row decisions only
+    if (kn.qk_format != BAPS_QK_BF16) return sp;                                       // bf16 Q/K only
     const long long flat = (long long)Sq * (Hq / Hkv);
     if (flat > 64) return sp;                                   // the prefill kernel's regime
     const long long tiles = (flat + 15) / 16;

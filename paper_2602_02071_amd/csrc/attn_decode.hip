@@ -51,6 +51,15 @@ template <int D>
 __device__ __forceinline__ int k_swz(int r) { return D == 128 ? (r & 15) : ((r >> 1) & 7); }
 template <int D>
 __device__ __forceinline__ int v_swz(int r) { return D == 128 ? 2 * (r & 3) : 2 * ((r >> 1) & 1); }
+// FP8 K rows (D bytes), read 16 rows at a time at one logical chunk
+template <int D>
+__device__ __forceinline__ int k8_swz(int r) { return D == 128 ? ((r ^ ((r >> 3) & 1)) & 7) : ((r >> 2) & 3); }
+
+typedef int i32x8 __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ i32x8 cat8(u32x4 a, u32x4 b)
+{
+    return i32x8{(int)a[0], (int)a[1], (int)a[2], (int)a[3], (int)b[0], (int)b[1], (int)b[2], (int)b[3]};
+}
 
 // One wave-wide asynchronous global->LDS load of 1 KiB, marked non-temporal:
 // every K/V byte is read once, so the stream should not displace cached data
@@ -62,10 +71,11 @@ __device__ __forceinline__ void lds_dma_16(const void* gptr, uint32_t lds_base)
                  : "memory", "m0");
 }
 
-// wait until at most n wave-wide loads of this wave are outstanding
+// wait until at most n wave-wide loads of this wave are outstanding (n is
+// rounded down to a multiple of 4: waiting longer is always safe)
 __device__ __forceinline__ void wait_vm(int n)
 {
-    switch (n) {
+    switch (n < 0 ? 0 : (n > 60 ? 60 : (n & ~3))) {
 #define W(N) case N: __builtin_amdgcn_s_waitcnt(0xF70 | ((N) & 15) | ((((N) >> 4) & 3) << 14)); break;
         W(0) W(4) W(8) W(12) W(16) W(20) W(24) W(28) W(32) W(36) W(40) W(44) W(48) W(52) W(56) W(60)
 #undef W
@@ -73,7 +83,7 @@ __device__ __forceinline__ void wait_vm(int n)
     }
 }
 
-template <int D, int BLK, bool CT, int MODE>
+template <int D, int BLK, bool CT, int MODE, bool F8>
 __global__ __launch_bounds__(64 * (BLK / 32)) void baps_attn_decode_kernel(AttnParams p)
 {
     static_assert(MODE == kModeE2E || CT, "the eq. (2) setups use the compact table (T <= 0)");
@@ -105,7 +115,9 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void baps_attn_decode_kernel(AttnP
     const int g = blockIdx.y;
     const int b = blockIdx.z;
     const uint16_t* kbase = p.k + ((long long)b * p.Hkv + g) * (long long)p.Sk * D;
+    const uint8_t* kbase8 = reinterpret_cast<const uint8_t*>(p.k) + ((long long)b * p.Hkv + g) * (long long)p.Sk * D;
     const uint16_t* vbase = p.v + ((long long)b * p.Hkv + g) * (long long)p.Sk * D;
+    constexpr int kIPS8 = kSlotKeys * D / 1024;   // loads of an FP8 K slot (half a slot)
 
     const int off = p.Sk - p.Sq;
     const int f_last = min(flat_rows - 1, tile * kRows + kRows - 1);
@@ -120,8 +132,18 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void baps_attn_decode_kernel(AttnP
         const int jb = n >> 1;
         const bool is_v = (n & 1) != 0;
         const int key0 = jb * BLK + wave * kSlotKeys;
-        const uint16_t* base = is_v ? vbase : kbase;
         const uint32_t dst = my_ring_lds + (uint32_t)((n % RW) * C::kSlotBytes);
+        if (F8 && !is_v) {                        // FP8 K: rows of D bytes
+#pragma unroll
+            for (int t = 0; t < kIPS8; ++t) {
+                const int r = t * (1024 / D) + lane / (D / 16);
+                const int ch = (lane % (D / 16)) ^ k8_swz<D>(r);
+                const int key = min(key0 + r, p.Sk - 1);
+                lds_dma_16(kbase8 + (long long)key * D + ch * 16, dst + t * 1024);
+            }
+            return;
+        }
+        const uint16_t* base = is_v ? vbase : kbase;
 #pragma unroll
         for (int t = 0; t < C::kIPS; ++t) {
             const int r = t * (1024 / C::kRowBytes) + lane / C::kCPR;
@@ -167,8 +189,15 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void baps_attn_decode_kernel(AttnP
 
     // Q^T as the B operand of S^T = K Q^T (16x16x32): lane holds
     // Q[row][32*kk + 8*grp .. +8]; K uses the same d order
-    u32x4 qop[kDK];
-    {
+    // (FP8: one 16x16x128 MFMA, lane holds Q[row][32*grp .. +32]; zeros past D)
+    u32x4 qop[F8 ? 1 : kDK];
+    i32x8 qop8 = {};
+    if constexpr (F8) {
+        const uint8_t* qrow = reinterpret_cast<const uint8_t*>(p.q) + (((long long)b * p.Hq + h) * p.Sq + r) * D;
+        if (row_ok && 32 * grp < D)
+            qop8 = cat8(*reinterpret_cast<const u32x4*>(qrow + 32 * grp),
+                        *reinterpret_cast<const u32x4*>(qrow + 32 * grp + 16));
+    } else {
         const uint16_t* qrow = p.q + (((long long)b * p.Hq + h) * p.Sq + r) * D;
 #pragma unroll
         for (int kk = 0; kk < kDK; ++kk)
@@ -194,7 +223,16 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void baps_attn_decode_kernel(AttnP
     const uint32_t vrow = vrow0 * C::kRowBytes + 2 * (vd0 & 7);
 
     int consumed = 0;
-    auto wait_slot = [&](int n) { wait_vm((issued - 1 - n) * C::kIPS); };
+    // loads issued after slot n (K slots are even; FP8 K slots carry kIPS8 loads)
+    auto wait_slot = [&](int n) {
+        if constexpr (F8) {
+            const int nv = issued / 2 - (n + 1) / 2;
+            const int nk = issued - 1 - n - nv;
+            wait_vm(nv * C::kIPS + nk * kIPS8);
+        } else {
+            wait_vm((issued - 1 - n) * C::kIPS);
+        }
+    };
     auto next_slot = [&]() {
         if (issued < nslots) { issue_slot(issued); ++issued; }
         ++consumed;
@@ -209,16 +247,31 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void baps_attn_decode_kernel(AttnP
         {
             wait_slot(consumed);
             const char* slot = my_ring + (consumed % RW) * C::kSlotBytes;
+            if constexpr (F8) {
+                // FP8 E4M3 K rows of D bytes; lane reads bytes [32 grp, +32) of key row 16 t2 + c16
+                const int kx8 = k8_swz<D>(c16);   // the same for rows c16 and 16 + c16
 #pragma unroll
-            for (int t2 = 0; t2 < 2; ++t2) {
-                f32x4 acc = {};
-#pragma unroll
-                for (int kk = 0; kk < kDK; ++kk) {
-                    const u32x4 a = *reinterpret_cast<const u32x4*>(
-                        slot + krow + t2 * 16 * C::kRowBytes + 16 * ((4 * kk + grp) ^ kx));
-                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a), as_bf16x8(qop[kk]), acc, 0, 0, 0);
+                for (int t2 = 0; t2 < 2; ++t2) {
+                    i32x8 a8 = {};
+                    if (32 * grp < D) {
+                        const char* kr = slot + (16 * t2 + c16) * D;
+                        a8 = cat8(*reinterpret_cast<const u32x4*>(kr + 16 * ((2 * grp) ^ kx8)),
+                                  *reinterpret_cast<const u32x4*>(kr + 16 * ((2 * grp + 1) ^ kx8)));
+                    }
+                    sacc[t2] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a8, qop8, f32x4{}, 0, 0, 0, 127, 0, 127);
                 }
-                sacc[t2] = acc;
+            } else {
+#pragma unroll
+                for (int t2 = 0; t2 < 2; ++t2) {
+                    f32x4 acc = {};
+#pragma unroll
+                    for (int kk = 0; kk < kDK; ++kk) {
+                        const u32x4 a = *reinterpret_cast<const u32x4*>(
+                            slot + krow + t2 * 16 * C::kRowBytes + 16 * ((4 * kk + grp) ^ kx));
+                        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a), as_bf16x8(qop[kk]), acc, 0, 0, 0);
+                    }
+                    sacc[t2] = acc;
+                }
             }
             next_slot();
         }
@@ -411,27 +464,33 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void baps_attn_decode_kernel(AttnP
     }
 }
 
-template <int D, int BLK, bool CT, int MODE>
+template <int D, int BLK, bool CT, int MODE, bool F8 = false>
 hipError_t launch_dec(const AttnParams& p, hipStream_t st)
 {
     using C = DCfg<D, BLK>;
     static_assert(C::kLdsBytes >= (C::kWaves - 1) * kRows * (D + 1) * 4, "merge buffer fits the ring");
     static bool attr_set = false;
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&baps_attn_decode_kernel<D, BLK, CT, MODE>),
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&baps_attn_decode_kernel<D, BLK, CT, MODE, F8>),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, C::kLdsBytes);
         if (e != hipSuccess) return e;
         attr_set = true;
     }
     const long long flat = (long long)p.Sq * (p.Hq / p.Hkv);
     const dim3 grid((unsigned)((flat + kRows - 1) / kRows), (unsigned)p.Hkv, (unsigned)p.B);
-    hipLaunchKernelGGL((baps_attn_decode_kernel<D, BLK, CT, MODE>), grid, dim3(64 * C::kWaves), C::kLdsBytes, st, p);
+    hipLaunchKernelGGL((baps_attn_decode_kernel<D, BLK, CT, MODE, F8>), grid, dim3(64 * C::kWaves), C::kLdsBytes, st, p);
     return hipGetLastError();
 }
 
 template <int D, int BLK>
 hipError_t launch_dec_ct(const AttnParams& p, hipStream_t st)
 {
+    if (p.qk_f8) {                                 // FP8 Q/K
+        if (p.mode == kModeDefault) return launch_dec<D, BLK, true, kModeDefault, true>(p, st);
+        if (p.mode == kModeExp2) return launch_dec<D, BLK, true, kModeExp2, true>(p, st);
+        if (p.lambda <= kCodeMaxLambda) return launch_dec<D, BLK, true, kModeE2E, true>(p, st);
+        return launch_dec<D, BLK, false, kModeE2E, true>(p, st);
+    }
     if (p.mode == kModeDefault) return launch_dec<D, BLK, true, kModeDefault>(p, st);
     if (p.mode == kModeExp2) return launch_dec<D, BLK, true, kModeExp2>(p, st);
     if (p.lambda <= kCodeMaxLambda) return launch_dec<D, BLK, true, kModeE2E>(p, st);

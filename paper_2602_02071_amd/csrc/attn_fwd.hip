@@ -50,6 +50,16 @@ template <int D>
 __device__ __forceinline__ int k_swz(int r) { return D == 128 ? (r & 15) : ((r >> 1) & 7); }
 template <int D>
 __device__ __forceinline__ int v_swz(int r) { return D == 128 ? 2 * (r & 3) : 2 * ((r >> 1) & 1); }
+// FP8 K rows (D bytes): 16 rows read at one logical chunk hit distinct banks,
+// and the swizzle of row 32*kt + j32 depends on j32 only
+template <int D>
+__device__ __forceinline__ int k8_swz(int r) { return D == 128 ? ((r ^ ((r >> 3) & 1)) & 7) : ((r >> 2) & 3); }
+
+typedef int i32x8 __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ i32x8 cat8(u32x4 a, u32x4 b)
+{
+    return i32x8{(int)a[0], (int)a[1], (int)a[2], (int)a[3], (int)b[0], (int)b[1], (int)b[2], (int)b[3]};
+}
 
 template <int D, int BLK, int NW>
 struct Cfg {
@@ -124,7 +134,22 @@ __device__ __forceinline__ void load_tile(const uint16_t* base, int key0, int Sk
     }
 }
 
-template <int D, int BLK, int NW, bool CT, int MODE, bool TILE>
+// The same for K in FP8 (rows of D bytes, half a bf16 tile).
+template <int D, int BLK, int NW>
+__device__ __forceinline__ void load_tile_k8(const uint8_t* base, int key0, int Sk, uint32_t lds_tile, int wave, int lane)
+{
+    constexpr int kCPR8 = D / 16;
+    constexpr int kLoads = BLK * D / 1024;
+#pragma unroll
+    for (int t = wave; t < kLoads; t += NW) {
+        const int r = t * (1024 / D) + lane / kCPR8;
+        const int c = (lane % kCPR8) ^ k8_swz<D>(r);
+        const int key = min(key0 + r, Sk - 1);
+        lds_dma_16(base + (long long)key * D + c * 16, __builtin_amdgcn_readfirstlane(lds_tile + t * 1024));
+    }
+}
+
+template <int D, int BLK, int NW, bool CT, int MODE, bool TILE, bool F8>
 __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
 {
     static_assert(MODE == kModeE2E || CT, "the eq. (2) setups use the compact table (T <= 0)");
@@ -178,6 +203,7 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
         b = hk / p.Hkv;
     }
     const uint16_t* kbase = p.k + ((long long)b * p.Hkv + g) * (long long)p.Sk * D;
+    const uint8_t* kbase8 = reinterpret_cast<const uint8_t*>(p.k) + ((long long)b * p.Hkv + g) * (long long)p.Sk * D;
     const uint16_t* vbase = p.v + ((long long)b * p.Hkv + g) * (long long)p.Sk * D;
 
     // key extent of the workgroup: its last row sees the most keys
@@ -187,7 +213,8 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
     const int nblk = kmax_tile < 0 ? 0 : kmax_tile / BLK + 1;
 
     if (nblk > 0) {
-        load_tile<D, BLK, NW, false>(kbase, 0, p.Sk, tiles_lds, wave, lane);
+        if constexpr (F8) load_tile_k8<D, BLK, NW>(kbase8, 0, p.Sk, tiles_lds, wave, lane);
+        else load_tile<D, BLK, NW, false>(kbase, 0, p.Sk, tiles_lds, wave, lane);
         load_tile<D, BLK, NW, true>(vbase, 0, p.Sk, tiles_lds + C::kTileBytes, wave, lane);
     }
     if constexpr (MODE == kModeDefault) {
@@ -242,8 +269,19 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
     }
 
     // Q^T as the B operand of S^T = K Q^T: lane holds Q[row][16*kk + 8*half .. +8]
-    u32x4 qop[kDK];
-    {
+    // (FP8: 32 bytes Q[row][64*kk + 32*half .. +32] per 32x32x64 MFMA)
+    constexpr int kDK8 = D / 64;
+    u32x4 qop[F8 ? 1 : kDK];
+    i32x8 qop8[F8 ? kDK8 : 1];
+    if constexpr (F8) {
+        const uint8_t* qrow = reinterpret_cast<const uint8_t*>(p.q) + (((long long)b * p.Hq + h) * p.Sq + r) * D;
+#pragma unroll
+        for (int kk = 0; kk < kDK8; ++kk) {
+            const u32x4 lo = row_ok ? *reinterpret_cast<const u32x4*>(qrow + 64 * kk + 32 * half) : u32x4{0, 0, 0, 0};
+            const u32x4 hi = row_ok ? *reinterpret_cast<const u32x4*>(qrow + 64 * kk + 32 * half + 16) : u32x4{0, 0, 0, 0};
+            qop8[kk] = cat8(lo, hi);
+        }
+    } else {
         const uint16_t* qrow = p.q + (((long long)b * p.Hq + h) * p.Sq + r) * D;
 #pragma unroll
         for (int kk = 0; kk < kDK; ++kk)
@@ -270,8 +308,14 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
     for (int t = 0; t < kDT; ++t) oacc[t] = f32x16{};
 
     // per-lane LDS byte offsets of the operand reads inside a tile
-    uint32_t koff[kDK];
-    {
+    uint32_t koff[F8 ? 2 * kDK8 : kDK];
+    if constexpr (F8) {
+        const int kx = k8_swz<D>(j32);           // FP8 rows of D bytes; two chunks per MFMA
+#pragma unroll
+        for (int kk = 0; kk < kDK8; ++kk)
+#pragma unroll
+            for (int e = 0; e < 2; ++e) koff[2 * kk + e] = j32 * D + 16 * ((4 * kk + 2 * half + e) ^ kx);
+    } else {
         const int kx = k_swz<D>(j32);            // swizzle of row kt*32 + j32 depends on j32 only
 #pragma unroll
         for (int kk = 0; kk < kDK; ++kk) koff[kk] = j32 * C::kRowBytes + 16 * ((2 * kk + half) ^ kx);
@@ -298,7 +342,8 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
         __syncthreads();                                    // everyone's did; block jb-1 fully consumed
         if (jb + 1 < nblk) {
             const uint32_t nk = tiles_lds + ((jb + 1) & 1) * 2 * C::kTileBytes;
-            load_tile<D, BLK, NW, false>(kbase, key0 + BLK, p.Sk, nk, wave, lane);
+            if constexpr (F8) load_tile_k8<D, BLK, NW>(kbase8, key0 + BLK, p.Sk, nk, wave, lane);
+            else load_tile<D, BLK, NW, false>(kbase, key0 + BLK, p.Sk, nk, wave, lane);
             load_tile<D, BLK, NW, true>(vbase, key0 + BLK, p.Sk, nk + C::kTileBytes, wave, lane);
         }
         if (key0 > kmax_wave_hi) {                          // nothing visible for this wave
@@ -318,13 +363,30 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
         f32x16 sacc[kKT];
 #pragma unroll
         for (int kt = 0; kt < kKT; ++kt) sacc[kt] = f32x16{};
+        if constexpr (F8) {
+            // FP8 E4M3 on both sides, unit block scales (E8M0 127): the
+            // dequantisation scales are folded into c
 #pragma unroll
-        for (int kk = 0; kk < kDK; ++kk) {
-            const char* kp = kt_lds + koff[kk];
+            for (int kk = 0; kk < kDK8; ++kk) {
 #pragma unroll
-            for (int kt = 0; kt < kKT; ++kt) {
-                const u32x4 a = *reinterpret_cast<const u32x4*>(kp + kt * 32 * C::kRowBytes);
-                sacc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(qop[kk]), sacc[kt], 0, 0, 0);
+                for (int kt = 0; kt < kKT; ++kt) {
+                    const char* kp = kt_lds + kt * 32 * D;
+                    const u32x4 lo = *reinterpret_cast<const u32x4*>(kp + koff[2 * kk]);
+                    const u32x4 hi = *reinterpret_cast<const u32x4*>(kp + koff[2 * kk + 1]);
+                    sacc[kt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(cat8(lo, hi), qop8[kk], sacc[kt],
+                                                                               0, 0, 0, 127, 0, 127);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int kk = 0; kk < kDK; ++kk) {
+                const char* kp = kt_lds + koff[kk];
+#pragma unroll
+                for (int kt = 0; kt < kKT; ++kt) {
+                    const u32x4 a = *reinterpret_cast<const u32x4*>(kp + kt * 32 * C::kRowBytes);
+                    sacc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(qop[kk]), sacc[kt],
+                                                                       0, 0, 0);
+                }
             }
         }
         __builtin_amdgcn_s_setprio(0);
@@ -536,21 +598,21 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
     }
 }
 
-template <int D, int BLK, int NW, bool CT, int MODE, bool TILE = false>
+template <int D, int BLK, int NW, bool CT, int MODE, bool TILE = false, bool F8 = false>
 hipError_t launch_one(const AttnParams& p, hipStream_t st)
 {
     using C = Cfg<D, BLK, NW>;
     static bool attr_set = false;
     if (!attr_set) {
         hipError_t e = hipFuncSetAttribute(
-            reinterpret_cast<const void*>(&baps_attn_fwd_kernel<D, BLK, NW, CT, MODE, TILE>),
+            reinterpret_cast<const void*>(&baps_attn_fwd_kernel<D, BLK, NW, CT, MODE, TILE, F8>),
             hipFuncAttributeMaxDynamicSharedMemorySize, C::kLdsBytes);
         if (e != hipSuccess) return e;
         attr_set = true;
     }
     const long long flat = (long long)p.Sq * (p.Hq / p.Hkv);
     const dim3 grid((unsigned)((flat + C::kTileRows - 1) / C::kTileRows), (unsigned)p.Hkv, (unsigned)p.B);
-    hipLaunchKernelGGL((baps_attn_fwd_kernel<D, BLK, NW, CT, MODE, TILE>), grid, dim3(C::kThreads), C::kLdsBytes,
+    hipLaunchKernelGGL((baps_attn_fwd_kernel<D, BLK, NW, CT, MODE, TILE, F8>), grid, dim3(C::kThreads), C::kLdsBytes,
                        st, p);
     return hipGetLastError();
 }
@@ -564,6 +626,12 @@ hipError_t launch_d_blk(const AttnParams& p, hipStream_t st)
     const int G = p.Hq / p.Hkv;
     const long long flat = (long long)p.Sq * G;
     if (flat <= 64 && (long long)p.restart_rows * G <= 16) return launch_attention_decode(p, D, BLK, st);
+    if (p.qk_f8) {                                 // FP8 Q/K (per-row restart only)
+        if (p.mode == kModeDefault) return launch_one<D, BLK, 8, true, kModeDefault, false, true>(p, st);
+        if (p.mode == kModeExp2) return launch_one<D, BLK, 8, true, kModeExp2, false, true>(p, st);
+        if (p.lambda <= kCodeMaxLambda) return launch_one<D, BLK, 8, true, kModeE2E, false, true>(p, st);
+        return launch_one<D, BLK, 8, false, kModeE2E, false, true>(p, st);
+    }
     if (p.mode == kModeDefault) return launch_one<D, BLK, 8, true, kModeDefault>(p, st);
     if (p.mode == kModeExp2) return launch_one<D, BLK, 8, true, kModeExp2>(p, st);
     if (p.restart_rows > 1) {

@@ -61,6 +61,7 @@ struct AttnParams {
     int mode;                   // kModeE2E, kModeDefault or kModeExp2
     int restart_rows;           // R: query positions of one head sharing the restart decision
     int b0_last;                // B0 also holds each row's last visible key block
+    int qk_f8;                  // q and k hold FP8 E4M3 codes (c already holds the scales)
     float c;                    // log2(e)/sqrt(D) as fp32 (or the caller's override)
 };
 

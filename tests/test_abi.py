@@ -127,3 +127,17 @@ def test_codec_and_softmax_block_argument_checks(lib):
     assert sb(16, 4, 100, 100, 64, 1, -1, 0, 16, 16, 16, 16, None, None) == 1    # n_b0
     assert sb(None, 4, 100, 100, 64, 1, 1, 0, 16, 16, 16, 16, None, None) == 1
     assert sb(None, 0, 100, 100, 64, 1, 1, 0, None, None, None, None, None, None) == 0
+
+
+def test_fp8_argument_checks(lib):
+    """FP8 Q/K: scales must be finite and positive, the format known, and
+    tile-level restart is not combined with it (no GPU work)."""
+    def ex(fmt, qs, ks, R=1):
+        prm = baps.baps_params_t(1, 1, 0.0, None, 0, R, 0, None, fmt, qs, ks)
+        return lib.baps_attention_fwd_ex(16, 16, 16, 16, None, 1, 8, 2, 64, 64, 128, 1, 128, ctypes.byref(prm), None)
+    assert ex(2, 1.0, 1.0) == 1                  # unknown format
+    assert ex(baps.BAPS_QK_FP8_E4M3, 0.0, 1.0) == 1
+    assert ex(baps.BAPS_QK_FP8_E4M3, 1.0, -2.0) == 1
+    assert ex(baps.BAPS_QK_FP8_E4M3, float("inf"), 1.0) == 1
+    assert ex(baps.BAPS_QK_FP8_E4M3, 1.0, 1.0, R=4) == 2
+    assert baps.baps_attention_split_workspace(1, 32, 8, 1, 32768, 128, 128, qk_scales=(1.0, 1.0)) == 0
