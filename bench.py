@@ -134,6 +134,47 @@ def softmax_setups(cfg, steps=20):
     return res
 
 
+def fp8_qk(steps=20):
+    """FP8 E4M3 Q/K (per-tensor scales) against bf16 on the same workloads:
+    the Llama-3-8B prefill (QK^T on the FP8 matrix cores: the dense peak of
+    the pass is 1 / (0.5/5.0 + 0.5/2.5) = 3.33 PFLOP/s with half the flop in
+    FP8 and half in bf16) and the batched decode (K streams half the bytes:
+    4*D - D bytes per key instead of 4*D)."""
+    import torch
+    import paper_2602_02071_amd as baps
+    from paper_2602_02071_amd.workloads import make_qk_fp8, make_workload
+    dev = torch.device("cuda:0")
+    out = {}
+    for cfg in (2, 3):
+        w, q, k, v = make_workload(cfg)
+        q8, k8, qs, ks = make_qk_fp8(q, k)
+        qt, kt, vt = (torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).to(dev) for x in (q, k, v))
+        q8t, k8t = (torch.from_numpy(np.ascontiguousarray(x)).to(dev) for x in (q8, k8))
+        o = torch.empty((w.B, w.Hq, w.Sq, w.D), dtype=torch.float32, device=dev)
+        lse = torch.empty((w.B, w.Hq, w.Sq), dtype=torch.float32, device=dev)
+        stream = torch.cuda.current_stream().cuda_stream
+        rec = {"workload": w.name, "q_scale": qs, "k_scale": ks}
+        for name, fn in (("bf16", lambda: baps.baps_attention_fwd(qt, kt, vt, o, lse, w.B, w.Hq, w.Hkv, w.Sq, w.Sk,
+                                                                    w.D, w.causal, w.block, stream)),
+                         ("fp8", lambda: baps.baps_attention_fwd_ex(q8t, k8t, vt, o, lse, w.B, w.Hq, w.Hkv, w.Sq, w.Sk,
+                                                                      w.D, w.causal, w.block, stream=stream,
+                                                                      qk_scales=(qs, ks)))):
+            _, per = _time_launches(fn, steps, 3, 50.0)
+            us = float(np.mean(per)) * 1e3
+            if w.Sq > 1:
+                tf = w.flops / (us * 1e-6) / 1e12
+                peak = PEAK_BF16_TFLOPS if name == "bf16" else 1.0 / (0.5 / 5000.0 + 0.5 / PEAK_BF16_TFLOPS)
+                rec[name] = {"us": us, "TFLOP/s": tf, "peak_TFLOP/s": peak, "frac": tf / peak}
+            else:
+                nb = w.bytes_qkvo
+                if name == "fp8":   # Q and K in one byte per element, V in two, O and lse in fp32
+                    nb = (w.B * w.Hq * w.Sq * w.D + w.B * w.Hkv * w.Sk * w.D * 3
+                          + w.B * w.Hq * w.Sq * (4 * w.D + 4))
+                rec[name] = {"us": us, "GB/s": nb / (us * 1e-6) / 1e9, "frac": nb / (us * 1e-6) / 1e9 / PEAK_HBM_GBS}
+        out[f"workload_{cfg}"] = rec
+    return out
+
+
 def restart_rates(cfgs=(2, 4, 3), lams=(0, 1, 2), tile_rows=64, steps=10):
     """The synthetic analogue of the paper's restart-rate table (Sec. 4.3,
     Table 4): per workload and lambda, the average restart rate (ARR:
@@ -282,6 +323,7 @@ def main():
     ap.add_argument("--no-boundary", action="store_true", help="skip the codec / softmax-block kernels")
     ap.add_argument("--no-modes", action="store_true", help="skip the Default / Exp2 HiF8 comparison")
     ap.add_argument("--no-restart-rates", action="store_true", help="skip the tile restart-rate table")
+    ap.add_argument("--no-fp8", action="store_true", help="skip the FP8 Q/K comparison")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -329,6 +371,8 @@ def main():
         out["softmax_setups"] = softmax_setups(args.config)
     if not args.no_restart_rates:
         out["restart_rates"] = restart_rates()
+    if not args.no_fp8:
+        out["fp8_qk"] = fp8_qk()
     if not args.no_decode and args.config != 3:
         out["decode_single_sequence"] = single_sequence_decode()
     if not args.no_boundary:
