@@ -134,6 +134,51 @@ __device__ __forceinline__ void load_tile(const uint16_t* base, int key0, int Sk
     }
 }
 
+// The wave's loads of a block that lies entirely before Sk (no clamp) with
+// the scalar-base form: lane offsets from the block's first row are fixed
+// per wave (precomputed once), the block's base address is wave-uniform, so
+// a load costs no vector instruction.
+__device__ __forceinline__ void lds_dma_16_sb(uint32_t voff, uint64_t sbase, uint32_t lds_base)
+{
+    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+                 :
+                 : "v"(voff), "s"(sbase), "s"(lds_base)
+                 : "memory", "m0");
+}
+
+__device__ __forceinline__ uint64_t uniform_addr(const void* p)
+{
+    const uint64_t a = (uint64_t)(uintptr_t)p;
+    return ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(a >> 32)) << 32) |
+           (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)a);
+}
+
+// per-load lane offsets (bytes from the block's first row) of this wave's
+// loads t = wave, wave + NW, ...; rows of RB bytes, CPR chunks of 16 bytes
+template <int NJ, int NW, int LOADS, int RB, int SWZ_KIND, int D>
+__device__ __forceinline__ void tile_offsets(uint32_t (&ofs)[NJ], int wave, int lane)
+{
+    constexpr int CPR = RB / 16;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+        const int t = wave + j * NW;
+        const int r = t * (1024 / RB) + lane / CPR;
+        const int sw = SWZ_KIND == 0 ? k_swz<D>(r) : (SWZ_KIND == 1 ? v_swz<D>(r) : k8_swz<D>(r));
+        ofs[j] = (uint32_t)(r * RB + 16 * ((lane % CPR) ^ sw));
+    }
+}
+
+template <int NJ, int NW, int LOADS>
+__device__ __forceinline__ void load_tile_sb(const void* block_base, const uint32_t (&ofs)[NJ], uint32_t lds_tile, int wave)
+{
+    const uint64_t sb = uniform_addr(block_base);
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+        const int t = wave + j * NW;
+        if (t < LOADS) lds_dma_16_sb(ofs[j], sb, __builtin_amdgcn_readfirstlane(lds_tile + t * 1024));
+    }
+}
+
 // The same for K in FP8 (rows of D bytes, half a bf16 tile).
 template <int D, int BLK, int NW>
 __device__ __forceinline__ void load_tile_k8(const uint8_t* base, int key0, int Sk, uint32_t lds_tile, int wave, int lane)
@@ -320,6 +365,14 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
 #pragma unroll
         for (int kk = 0; kk < kDK; ++kk) koff[kk] = j32 * C::kRowBytes + 16 * ((2 * kk + half) ^ kx);
     }
+    // lane offsets of the scalar-base K / V loads (blocks inside Sk)
+    constexpr int kLoadsK = F8 ? BLK * D / 1024 : C::kLoadsPerTile;
+    constexpr int kNJK = (kLoadsK + NW - 1) / NW;
+    constexpr int kNJV = (C::kLoadsPerTile + NW - 1) / NW;
+    uint32_t kdofs[kNJK], vdofs[kNJV];
+    tile_offsets<kNJK, NW, kLoadsK, F8 ? D : C::kRowBytes, F8 ? 2 : 0, D>(kdofs, wave, lane);
+    tile_offsets<kNJV, NW, C::kLoadsPerTile, C::kRowBytes, 1, D>(vdofs, wave, lane);
+
     uint32_t voff[kDT];
     {
         // transposing reads: lane l of a 16-lane group points at row
@@ -342,9 +395,16 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
         __syncthreads();                                    // everyone's did; block jb-1 fully consumed
         if (jb + 1 < nblk) {
             const uint32_t nk = tiles_lds + ((jb + 1) & 1) * 2 * C::kTileBytes;
-            if constexpr (F8) load_tile_k8<D, BLK, NW>(kbase8, key0 + BLK, p.Sk, nk, wave, lane);
-            else load_tile<D, BLK, NW, false>(kbase, key0 + BLK, p.Sk, nk, wave, lane);
-            load_tile<D, BLK, NW, true>(vbase, key0 + BLK, p.Sk, nk + C::kTileBytes, wave, lane);
+            const int k1 = key0 + BLK;
+            if (k1 + BLK <= p.Sk) {                         // the whole next block lies before Sk
+                if constexpr (F8) load_tile_sb<kNJK, NW, kLoadsK>(kbase8 + (long long)k1 * D, kdofs, nk, wave);
+                else load_tile_sb<kNJK, NW, kLoadsK>(kbase + (long long)k1 * D, kdofs, nk, wave);
+                load_tile_sb<kNJV, NW, C::kLoadsPerTile>(vbase + (long long)k1 * D, vdofs, nk + C::kTileBytes, wave);
+            } else {
+                if constexpr (F8) load_tile_k8<D, BLK, NW>(kbase8, k1, p.Sk, nk, wave, lane);
+                else load_tile<D, BLK, NW, false>(kbase, k1, p.Sk, nk, wave, lane);
+                load_tile<D, BLK, NW, true>(vbase, k1, p.Sk, nk + C::kTileBytes, wave, lane);
+            }
         }
         if (key0 > kmax_wave_hi) {                          // nothing visible for this wave
             if constexpr (TILE) {
