@@ -307,7 +307,55 @@ def cpu_baseline(w, qkv, seconds_hint=True):
     vis = np.minimum(w.Sk, r + w.Sk - w.Sq + 1) if w.causal else np.full(r.shape, w.Sk)
     flops = 4.0 * w.D * float(np.clip(vis, 0, w.Sk).sum())
     sample = f"{len(rows)} of {w.B * w.Hq * w.Sq} query rows ({what}), {dt:.1f} s"
-    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": nthreads, "kind": "oracle", "sample": sample}
+    # one thread on every 16th row of the same sample
+    rows1 = rows[::16]
+    t0 = time.perf_counter()
+    oracle.attention(q, k, v, w.B, w.Hq, w.Hkv, w.Sq, w.Sk, w.D, w.causal, w.block, rows=rows1, nthreads=1)
+    dt1 = time.perf_counter() - t0
+    r1 = rows1 % w.Sq
+    vis1 = np.minimum(w.Sk, r1 + w.Sk - w.Sq + 1) if w.causal else np.full(r1.shape, w.Sk)
+    flops1 = 4.0 * w.D * float(np.clip(vis1, 0, w.Sk).sum())
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": nthreads, "kind": "oracle", "sample": sample,
+            "cpu_model": model, "affinity_cores": len(os.sched_getaffinity(0)),
+            "single_thread": {"value": flops1 / dt1 / 1e12, "unit": "TFLOP/s",
+                              "sample": f"{len(rows1)} rows (every 16th of the sample), {dt1:.1f} s"}}
+
+
+def other_workloads(cfgs=(4, 5), steps=5):
+    """The other MFMA-bound workloads of the benchmark set at full size: the
+    ViT/multimodal encoder (B8 H16 S4096 D64, non-causal, block 64) and the
+    long-context prefill (B1 Hq32 Hkv8 S32768 D128, causal, outlier channels
+    and an attention sink, block 128).  Per-launch mean, algorithmic TFLOP/s
+    and tokens/s, against 2.5 PFLOP/s dense bf16."""
+    import torch
+    import paper_2602_02071_amd as baps
+    from paper_2602_02071_amd.workloads import make_workload
+    dev = torch.device("cuda:0")
+    out = {}
+    for cfg in cfgs:
+        w, q, k, v = make_workload(cfg)
+        qt, kt, vt = (torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).to(dev) for x in (q, k, v))
+        o = torch.empty((w.B, w.Hq, w.Sq, w.D), dtype=torch.float32, device=dev)
+        lse = torch.empty((w.B, w.Hq, w.Sq), dtype=torch.float32, device=dev)
+        stream = torch.cuda.current_stream().cuda_stream
+
+        def step():
+            baps.baps_attention_fwd(qt, kt, vt, o, lse, w.B, w.Hq, w.Hkv, w.Sq, w.Sk, w.D, w.causal, w.block, stream)
+        _, per = _time_launches(step, steps, 2, 100.0)
+        ms = float(np.mean(per))
+        tf = w.flops / (ms * 1e-3) / 1e12
+        out[f"workload_{cfg}"] = {"workload": w.name, "us": ms * 1e3, "TFLOP/s": tf, "frac": tf / PEAK_BF16_TFLOPS,
+                                  "tokens_per_s": w.B * w.Sq / (ms * 1e-3)}
+        del qt, kt, vt, o, lse
+    return out
 
 
 def main():
@@ -324,6 +372,7 @@ def main():
     ap.add_argument("--no-modes", action="store_true", help="skip the Default / Exp2 HiF8 comparison")
     ap.add_argument("--no-restart-rates", action="store_true", help="skip the tile restart-rate table")
     ap.add_argument("--no-fp8", action="store_true", help="skip the FP8 Q/K comparison")
+    ap.add_argument("--no-other", action="store_true", help="skip the ViT and long-prefill workloads")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -373,6 +422,8 @@ def main():
         out["restart_rates"] = restart_rates()
     if not args.no_fp8:
         out["fp8_qk"] = fp8_qk()
+    if not args.no_other and args.config == 2:
+        out["other_workloads"] = other_workloads()
     if not args.no_decode and args.config != 3:
         out["decode_single_sequence"] = single_sequence_decode()
     if not args.no_boundary:
