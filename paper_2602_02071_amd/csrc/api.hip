@@ -251,7 +251,6 @@ SplitPlan split_plan(int B, int Hq, int Hkv, int Sq, int Sk, int D, int block, c
     if (!(D == 64 || D == 128) || !(block == 32 || block == 64 || block == 128)) return sp;
     if (kn.mode != BAPS_MODE_E2E_HIF8 || kn.lambda > kCodeMaxLambda) return sp;
     if (kn.restart_rows < 0 || effective_rows(kn.restart_rows, Sq) > 1) return sp;   // per-row decisions only
-    if (kn.qk_format != BAPS_QK_BF16) return sp;                                       // bf16 Q/K only
     const long long flat = (long long)Sq * (Hq / Hkv);
     if (flat > 64) return sp;                                   // the prefill kernel's regime
     const long long tiles = (flat + 15) / 16;

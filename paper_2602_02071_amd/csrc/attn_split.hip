@@ -52,6 +52,15 @@ template <int D>
 __device__ __forceinline__ int k_swz(int r) { return D == 128 ? (r & 15) : ((r >> 1) & 7); }
 template <int D>
 __device__ __forceinline__ int v_swz(int r) { return D == 128 ? 2 * (r & 3) : 2 * ((r >> 1) & 1); }
+// FP8 K rows (D bytes), read 16 rows at a time at one logical chunk
+template <int D>
+__device__ __forceinline__ int k8_swz(int r) { return D == 128 ? ((r ^ ((r >> 3) & 1)) & 7) : ((r >> 2) & 3); }
+
+typedef int i32x8 __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ i32x8 cat8(u32x4 a, u32x4 b)
+{
+    return i32x8{(int)a[0], (int)a[1], (int)a[2], (int)a[3], (int)b[0], (int)b[1], (int)b[2], (int)b[3]};
+}
 
 // one wave-wide non-temporal global->LDS load of 1 KiB (every byte read once)
 __device__ __forceinline__ void lds_dma_16(const void* gptr, uint32_t lds_base)
@@ -97,7 +106,7 @@ __device__ __forceinline__ RowInfo row_info(const AttnParams& p, int tile, int g
 // ---------------------------------------------------------------------------
 // 1. scores: acc and block maxima of one key split
 // ---------------------------------------------------------------------------
-template <int D, int BLK>
+template <int D, int BLK, bool F8>
 __global__ __launch_bounds__(64 * (BLK / 32)) void split_scores_kernel(SplitParams sp)
 {
     using C = SCfg<D, BLK>;
@@ -121,15 +130,27 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void split_scores_kernel(SplitPara
     const int flat = p.Sq * (p.Hq / p.Hkv);
     const long long bg = (long long)b * p.Hkv + g;
     const uint16_t* kbase = p.k + bg * (long long)p.Sk * D;
+    const uint8_t* kbase8 = reinterpret_cast<const uint8_t*>(p.k) + bg * (long long)p.Sk * D;
     const int j0 = split * sp.bps;
     const int j1 = min(sp.nblk, j0 + sp.bps);
     const int nslots = max(0, j1 - j0);
+    constexpr int kIPS = F8 ? kSlotKeys * D / 1024 : C::kIPS;     // loads per slot (FP8 K: rows of D bytes)
 
     const uint32_t my_ring_lds = ring_lds + (uint32_t)(wave * RW * C::kSlotBytes);
     const char* my_ring = ring + wave * RW * C::kSlotBytes;
     auto issue_slot = [&](int n) {               // K keys [32*wave, +32) of block j0 + n
         const int key0 = (j0 + n) * BLK + wave * kSlotKeys;
         const uint32_t dst = my_ring_lds + (uint32_t)((n % RW) * C::kSlotBytes);
+        if constexpr (F8) {
+#pragma unroll
+            for (int t = 0; t < kIPS; ++t) {
+                const int rr = t * (1024 / D) + lane / (D / 16);
+                const int ch = (lane % (D / 16)) ^ k8_swz<D>(rr);
+                const int key = min(key0 + rr, p.Sk - 1);
+                lds_dma_16(kbase8 + (long long)key * D + ch * 16, dst + t * 1024);
+            }
+            return;
+        }
 #pragma unroll
         for (int t = 0; t < C::kIPS; ++t) {
             const int rr = t * (1024 / C::kRowBytes) + lane / C::kCPR;
@@ -146,8 +167,14 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void split_scores_kernel(SplitPara
 #pragma unroll
     for (int o = 1; o < 16; o <<= 1) kmax_lo = min(kmax_lo, __shfl_xor(kmax_lo, o, 64));
     kmax_lo = __builtin_amdgcn_readfirstlane(kmax_lo);
-    u32x4 qop[kDK];
-    {
+    u32x4 qop[F8 ? 1 : kDK];
+    i32x8 qop8 = {};                              // FP8: Q[row][32*grp .. +32], zeros past D
+    if constexpr (F8) {
+        const uint8_t* qrow = reinterpret_cast<const uint8_t*>(p.q) + (((long long)b * p.Hq + ri.h) * p.Sq + ri.r) * D;
+        if (ri.ok && 32 * grp < D)
+            qop8 = cat8(*reinterpret_cast<const u32x4*>(qrow + 32 * grp),
+                        *reinterpret_cast<const u32x4*>(qrow + 32 * grp + 16));
+    } else {
         const uint16_t* qrow = p.q + (((long long)b * p.Hq + ri.h) * p.Sq + ri.r) * D;
 #pragma unroll
         for (int kk = 0; kk < kDK; ++kk)
@@ -164,18 +191,32 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void split_scores_kernel(SplitPara
         const int jb = j0 + n;
         const int key0 = jb * BLK + wave * kSlotKeys;
         f32x4 sacc[2];
-        wait_vm((issued - 1 - n) * C::kIPS);
+        wait_vm((issued - 1 - n) * kIPS);
         const char* slot = my_ring + (n % RW) * C::kSlotBytes;
+        if constexpr (F8) {
+            const int kx8 = k8_swz<D>(c16);
 #pragma unroll
-        for (int t2 = 0; t2 < 2; ++t2) {
-            f32x4 a4 = {};
-#pragma unroll
-            for (int kk = 0; kk < kDK; ++kk) {
-                const u32x4 a = *reinterpret_cast<const u32x4*>(
-                    slot + krow + t2 * 16 * C::kRowBytes + 16 * ((4 * kk + grp) ^ kx));
-                a4 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a), as_bf16x8(qop[kk]), a4, 0, 0, 0);
+            for (int t2 = 0; t2 < 2; ++t2) {
+                i32x8 a8 = {};
+                if (32 * grp < D) {
+                    const char* kr = slot + (16 * t2 + c16) * D;
+                    a8 = cat8(*reinterpret_cast<const u32x4*>(kr + 16 * ((2 * grp) ^ kx8)),
+                              *reinterpret_cast<const u32x4*>(kr + 16 * ((2 * grp + 1) ^ kx8)));
+                }
+                sacc[t2] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a8, qop8, f32x4{}, 0, 0, 0, 127, 0, 127);
             }
-            sacc[t2] = a4;
+        } else {
+#pragma unroll
+            for (int t2 = 0; t2 < 2; ++t2) {
+                f32x4 a4 = {};
+#pragma unroll
+                for (int kk = 0; kk < kDK; ++kk) {
+                    const u32x4 a = *reinterpret_cast<const u32x4*>(
+                        slot + krow + t2 * 16 * C::kRowBytes + 16 * ((4 * kk + grp) ^ kx));
+                    a4 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a), as_bf16x8(qop[kk]), a4, 0, 0, 0);
+                }
+                sacc[t2] = a4;
+            }
         }
         if (issued < nslots) { issue_slot(issued); ++issued; }
         // mask keys past kmax; register i of tile t2 holds key key0 + 16*t2 + 4*grp + i
@@ -588,8 +629,11 @@ hipError_t launch_split_db(const SplitParams& sp, hipStream_t st)
     static_assert(C::kLdsBytes >= (C::kWaves - 1) * kRows * (D + 1) * 4, "merge buffer fits the ring");
     static bool attr_set = false;
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&split_scores_kernel<D, BLK>),
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&split_scores_kernel<D, BLK, false>),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, C::kLdsBytes);
+        if (e == hipSuccess)
+            e = hipFuncSetAttribute(reinterpret_cast<const void*>(&split_scores_kernel<D, BLK, true>),
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, C::kLdsBytes);
         if (e == hipSuccess)
             e = hipFuncSetAttribute(reinterpret_cast<const void*>(&split_pv_kernel<D, BLK>),
                                     hipFuncAttributeMaxDynamicSharedMemorySize, PC::kLdsBytes);
@@ -603,7 +647,10 @@ hipError_t launch_split_db(const SplitParams& sp, hipStream_t st)
     const long long flat = (long long)p.Sq * (p.Hq / p.Hkv);
     const unsigned tiles = (unsigned)((flat + kRows - 1) / kRows);
     const dim3 grid(tiles * (unsigned)sp.nsplit, (unsigned)p.Hkv, (unsigned)p.B);
-    hipLaunchKernelGGL((split_scores_kernel<D, BLK>), grid, dim3(64 * C::kWaves), C::kLdsBytes, st, sp);
+    if (p.qk_f8)
+        hipLaunchKernelGGL((split_scores_kernel<D, BLK, true>), grid, dim3(64 * C::kWaves), C::kLdsBytes, st, sp);
+    else
+        hipLaunchKernelGGL((split_scores_kernel<D, BLK, false>), grid, dim3(64 * C::kWaves), C::kLdsBytes, st, sp);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((split_pv_kernel<D, BLK>), grid, dim3(PC::kThreads), PC::kLdsBytes, st, sp);

@@ -140,4 +140,4 @@ def test_fp8_argument_checks(lib):
     assert ex(baps.BAPS_QK_FP8_E4M3, 1.0, -2.0) == 1
     assert ex(baps.BAPS_QK_FP8_E4M3, float("inf"), 1.0) == 1
     assert ex(baps.BAPS_QK_FP8_E4M3, 1.0, 1.0, R=4) == 2
-    assert baps.baps_attention_split_workspace(1, 32, 8, 1, 32768, 128, 128, qk_scales=(1.0, 1.0)) == 0
+    assert baps.baps_attention_split_workspace(1, 32, 8, 1, 32768, 128, 128, qk_scales=(1.0, 1.0)) > 0

@@ -83,3 +83,25 @@ def test_fp8_softmax_setups(mode, case):
 def test_fp8_knobs(lam, n_b0, b0_last):
     _run((1, 8, 2, 128, 400, 128, True), 128, seed=lam + 60, lam=lam, n_b0=n_b0, b0_last=b0_last)
     _run((2, 8, 2, 1, 700, 128, False), 128, seed=lam + 61, lam=lam, n_b0=n_b0, b0_last=b0_last)
+
+
+@pytest.mark.parametrize("shape,block", [((1, 32, 8, 1, 32768, 128, False), 128), ((1, 8, 2, 1, 5077, 64, False), 64),
+                                         ((1, 4, 1, 8, 3000, 128, True), 128)])
+def test_split_fp8(shape, block):
+    """The split-key path with FP8 K: the same dot products as the one-pass
+    decode kernel (both take 16x16x128), so the same result to fp32
+    summation order, and the oracle's parity bar."""
+    import torch
+    import paper_2602_02071_amd as baps
+    B, Hq, Hkv, Sq, Sk, D, causal = shape
+    assert baps.baps_attention_split_workspace(B, Hq, Hkv, Sq, Sk, D, block, qk_scales=(1.0, 1.0)) > 0
+    q, k, v = make_qkv(B, Hq, Hkv, Sq, Sk, D, seed=sum(shape) + 3, outliers=False, lognormal_k=True)
+    q8, k8, qs, ks = make_qk_fp8(q, k)
+    args = (_dev_u8(q8), _dev_u8(k8), dev_bf16(v), causal, block)
+    o, lse = baps.attention(*args, split=True, qk_scales=(qs, ks))
+    o1, _ = baps.attention(*args, qk_scales=(qs, ks))
+    torch.cuda.synchronize()
+    assert float((o - o1).abs().max()) <= 2e-5 * max(1.0, float(o1.abs().max()))
+    check_parity(O.e4m3_to_bf16(q8), O.e4m3_to_bf16(k8), v, shape, block, o.cpu().numpy().reshape(-1, D).astype(np.float64),
+                 lse.cpu().numpy().reshape(-1).astype(np.float64), label=f"split fp8 {shape}",
+                 scale_log2=O.fp8_scale_log2(D, qs, ks), qk_fp8=True)
