@@ -202,9 +202,10 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
     static_assert(D == 64 || D == 128, "head dimension");
     static_assert(BLK % 32 == 0 && BLK <= 128, "key block");
     using C = Cfg<D, BLK, NW>;
-    // P lookup: the compact code table (lambda <= kCodeMaxLambda), else the
-    // bf16 half of the full score table
-    __shared__ __attribute__((aligned(16))) uint8_t ctab[CT ? kCodeHi + 1 : 1];
+    // P lookup: the code table (lambda <= kCodeMaxLambda) expanded to all
+    // 8192 indices, so that a lookup needs no clamp; else the bf16 half of the
+    // full score table
+    __shared__ __attribute__((aligned(16))) uint8_t ctab[CT ? kTabEntries : 1];
     __shared__ __attribute__((aligned(16))) uint16_t tab[CT ? 1 : kTabEntries];
     __shared__ uint32_t tflag[TILE ? NW : 1][3];  // per wave: rows that restart, see the block, are in B0
     extern __shared__ __attribute__((aligned(1024))) char tiles[];
@@ -265,7 +266,9 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
     if constexpr (MODE == kModeDefault) {
         // fp32 exp2: no table
     } else if constexpr (CT) {
-        for (int i = tid; i < kCodeEntries; i += C::kThreads) ctab[kCodeLo + i] = p.ctab[i];
+        // indices below kCodeLo take the entry of kCodeLo (P = 1), above
+        // kCodeHi that of kCodeHi (P = 0)
+        for (int i = tid; i < kTabEntries; i += C::kThreads) ctab[i] = p.ctab[min(max(i, kCodeLo), kCodeHi) - kCodeLo];
     } else {
         for (int i = tid; i < kTabEntries; i += C::kThreads) tab[i] = (uint16_t)(p.tab[i] >> 16);
     }
@@ -438,6 +441,7 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
                 }
             }
         } else {
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int kk = 0; kk < kDK; ++kk) {
                 const char* kp = kt_lds + koff[kk];
@@ -448,6 +452,18 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
                                                                        0, 0, 0);
                 }
             }
+            // keep kKReads operand reads in flight ahead of the MFMAs that
+            // consume them (the default schedule keeps two, and the MFMAs
+            // wait on LDS latency)
+            constexpr int kKReads = 4;
+            __builtin_amdgcn_sched_group_barrier(0x100, kKReads, 0);          // LDS reads
+#pragma unroll
+            for (int i = 0; i < kDK * kKT - kKReads; ++i) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);            // one MFMA
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);            // one LDS read
+            }
+            __builtin_amdgcn_sched_group_barrier(0x008, kKReads, 0);
+            __builtin_amdgcn_sched_barrier(0);
         }
         __builtin_amdgcn_s_setprio(0);
         // mask keys past kmax (causal diagonal, ragged tail); key of register
@@ -551,8 +567,7 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
                 if constexpr (MODE == kModeDefault) {
                     f = __builtin_amdgcn_exp2f(x);
                 } else {
-                    const uint32_t ix = min(max(hif8::f2u(x) >> kTabShift, (uint32_t)kCodeLo), (uint32_t)kCodeHi);
-                    f = hif8::u2f((uint32_t)ctab[ix] << 20) * 0x1p104f;
+                    f = hif8::u2f((uint32_t)ctab[hif8::f2u(x) >> kTabShift] << 20) * 0x1p104f;
                 }
             }
             if (__any(f != 1.0f)) {
@@ -596,9 +611,7 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
                                                       : sacc[kt][ch * 8 + 2 * e + 1] * c + nref;
                     if constexpr (CT) {
                         // two bf16 of P * 2^-kCodeBiasLog2
-                        const uint32_t i0 = min(max(hif8::f2u(t0) >> kTabShift, (uint32_t)kCodeLo), (uint32_t)kCodeHi);
-                        const uint32_t i1 = min(max(hif8::f2u(t1) >> kTabShift, (uint32_t)kCodeLo), (uint32_t)kCodeHi);
-                        w = ((uint32_t)ctab[i0] | ((uint32_t)ctab[i1] << 16)) << 4;
+                        w = ((uint32_t)ctab[hif8::f2u(t0) >> kTabShift] | ((uint32_t)ctab[hif8::f2u(t1) >> kTabShift] << 16)) << 4;
                     } else {
                         w = (uint32_t)tab[hif8::f2u(t0) >> kTabShift] | ((uint32_t)tab[hif8::f2u(t1) >> kTabShift] << 16);
                     }

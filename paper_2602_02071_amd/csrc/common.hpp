@@ -30,7 +30,9 @@ constexpr int kTabShift = 19;
 // that c << 4 is the bf16 pattern of P * 2^-kCodeBiasLog2, exactly: e runs
 // over [-22, kCodeMaxLambda] and HiF8 keeps at most 3 mantissa bits.  In
 // practice the hit entries sit in a few dozen LDS dwords: the gathers are
-// free of bank conflicts.
+// nearly free of bank conflicts.  The prefill kernel expands the table in LDS
+// to all 8192 indices (entry kCodeLo below, kCodeHi above the range), which
+// takes the clamp off every lookup.
 constexpr int kCodeLo = 0x7A0;           // T = +2^-5
 constexpr int kCodeHi = 0x1840;          // T = -32
 constexpr int kCodeEntries = kCodeHi - kCodeLo + 1;
