@@ -409,23 +409,23 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
                 load_tile<D, BLK, NW, true>(vbase, k1, p.Sk, nk + C::kTileBytes, wave, lane);
             }
         }
-        if (key0 > kmax_wave_hi) {                          // nothing visible for this wave
-            if constexpr (TILE) {
-                if (xwave) {                                // it still takes part in the tile exchange
-                    if (lane == 0) tflag[wave][0] = tflag[wave][1] = tflag[wave][2] = 0u;
-                    __syncthreads();
-                }
-            }
-            continue;
-        }
+        // A wave that sees nothing of the block skips it.  In a tile that
+        // spans waves it still takes part in the tile's exchange below, with
+        // no visible row (its row maximum stays -inf): the exchange has one
+        // barrier on one path, and the tile's representative lane counts the
+        // block whenever any row of the tile sees it.
+        const bool live = key0 <= kmax_wave_hi;
+        if (!live && !(TILE && xwave)) continue;
 
+        f32x16 sacc[kKT];
+#pragma unroll
+        for (int kt = 0; kt < kKT; ++kt) sacc[kt] = f32x16{};
+        float amax = ninf;
+        if (live) {
         // S^T = K_j Q^T.  The wave raises its priority for the MFMA burst so
         // that the two waves sharing a SIMD drift apart: one runs its QK^T
         // MFMAs while the other runs the VALU softmax of its block.
         __builtin_amdgcn_s_setprio(2);
-        f32x16 sacc[kKT];
-#pragma unroll
-        for (int kt = 0; kt < kKT; ++kt) sacc[kt] = f32x16{};
         if constexpr (F8) {
             // FP8 E4M3 on both sides, unit block scales (E8M0 127): the
             // dequantisation scales are folded into c
@@ -479,7 +479,6 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
         }
         // row maximum of the raw dot products (the scale c > 0 is monotone):
         // a 3-way tree over this lane's 16*kKT scores, then lanes l and l^32
-        float amax;
         {
             float mx[16 * kKT];
 #pragma unroll
@@ -489,6 +488,7 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
             amax = tree_max<16 * kKT>(mx);
             amax = __builtin_fmaxf(amax, swap_halves(amax));
         }
+        }  // live
 
         float nref;
         if constexpr (MODE == kModeE2E) {
@@ -582,6 +582,7 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
             nref = (m == ninf) ? 0.0f : -m;
         }
 
+        if (!live) continue;
         const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 #pragma unroll
         for (int kt = 0; kt < kKT; ++kt) {

@@ -69,7 +69,13 @@ def test_decode_tiles(case, b0_last):
 
 @pytest.mark.parametrize("shape,block,R", [((1, 8, 2, 256, 512, 128, True), 128, 16),
                                            ((2, 8, 2, 4, 2000, 128, True), 128, 4),
-                                           ((1, 8, 2, 64, 700, 64, True), 64, 1)])
+                                           ((1, 8, 2, 64, 700, 64, True), 64, 1),
+                                           # ragged causal offsets: a block boundary falls
+                                           # inside a tile that spans two waves, so the
+                                           # tile's first wave sees nothing of a block its
+                                           # second wave sees
+                                           ((1, 8, 2, 250, 512, 128, True), 128, 16),
+                                           ((1, 4, 4, 300, 301, 128, True), 128, 64)])
 def test_tile_counters(shape, block, R):
     """Per-tile restarted / visited B1 blocks against the oracle: equal on
     every tile whose decisions are clear of a rounding boundary."""
