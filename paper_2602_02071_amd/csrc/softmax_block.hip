@@ -161,13 +161,17 @@ __device__ __forceinline__ float row16_sum(float v)
 }
 
 constexpr int kRowsPerWave4 = 4;
-constexpr int kRows4PerBlock = kRowsPerWave4 * (kThreads / 64);
 
-template <int BLOCK>
-__global__ __launch_bounds__(kThreads) void softmax_block4_kernel(SoftmaxBlockParams p)
+// NT threads per workgroup, 4 rows per wave.  With rows enough to give every
+// CU a workgroup, 1024 threads (64 rows, one workgroup and one 32 KiB table
+// copy per CU) run about 10 % faster than 256 threads (four workgroups and
+// four table copies per CU).
+template <int BLOCK, int NT>
+__global__ __launch_bounds__(NT) void softmax_block4_kernel(SoftmaxBlockParams p)
 {
+    constexpr int kRows4PerBlock = kRowsPerWave4 * (NT / 64);
     __shared__ uint32_t tab[kTabEntries];
-    for (int i = threadIdx.x; i < kTabEntries; i += kThreads) tab[i] = p.tab[i];
+    for (int i = threadIdx.x; i < kTabEntries; i += NT) tab[i] = p.tab[i];
     __syncthreads();
 
     constexpr int kCh = BLOCK < 256 ? 256 : BLOCK;        // columns per row per step
@@ -270,6 +274,19 @@ __global__ __launch_bounds__(kThreads) void softmax_block4_kernel(SoftmaxBlockPa
     }
 }
 
+template <int NT>
+hipError_t launch_block4(const SoftmaxBlockParams& p, hipStream_t st)
+{
+    constexpr int kRows4PerBlock = kRowsPerWave4 * (NT / 64);
+    const dim3 grid4((unsigned)((p.rows + kRows4PerBlock - 1) / kRows4PerBlock));
+    switch (p.block) {
+    case 64: hipLaunchKernelGGL((softmax_block4_kernel<64, NT>), grid4, dim3(NT), 0, st, p); break;
+    case 128: hipLaunchKernelGGL((softmax_block4_kernel<128, NT>), grid4, dim3(NT), 0, st, p); break;
+    default: hipLaunchKernelGGL((softmax_block4_kernel<256, NT>), grid4, dim3(NT), 0, st, p); break;
+    }
+    return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_softmax_block(const SoftmaxBlockParams& p, hipStream_t st)
@@ -277,13 +294,19 @@ hipError_t launch_softmax_block(const SoftmaxBlockParams& p, hipStream_t st)
     const bool vec = ((uintptr_t)p.s % 16 == 0) && (p.ld % 4 == 0) && (p.cols % 4 == 0) &&
                      ((uintptr_t)p.codes % 4 == 0) && p.block <= 256;
     if (vec) {
-        const dim3 grid4((unsigned)((p.rows + kRows4PerBlock - 1) / kRows4PerBlock));
-        switch (p.block) {
-        case 64: hipLaunchKernelGGL(softmax_block4_kernel<64>, grid4, dim3(kThreads), 0, st, p); break;
-        case 128: hipLaunchKernelGGL(softmax_block4_kernel<128>, grid4, dim3(kThreads), 0, st, p); break;
-        default: hipLaunchKernelGGL(softmax_block4_kernel<256>, grid4, dim3(kThreads), 0, st, p); break;
+        // one 1024-thread workgroup per CU when the rows fill every CU
+        static int ncu_of[64] = {};                 // CU count per device, read once
+        int dev = 0;
+        hipError_t e = hipGetDevice(&dev);
+        if (e != hipSuccess) return e;
+        int ncu = (dev >= 0 && dev < 64) ? ncu_of[dev] : 0;
+        if (ncu == 0) {
+            e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
+            if (e != hipSuccess) return e;
+            if (dev >= 0 && dev < 64) ncu_of[dev] = ncu;
         }
-        return hipGetLastError();
+        const long long wg1024 = (p.rows + 4 * 16 - 1) / (4 * 16);
+        return wg1024 >= ncu ? launch_block4<1024>(p, st) : launch_block4<256>(p, st);
     }
     const dim3 grid((unsigned)((p.rows + kRowsPerBlock - 1) / kRowsPerBlock));
     switch (p.block) {

@@ -100,3 +100,12 @@ def test_row_group_path_many_blocks(block, cols):
     s[5, :] = -np.inf
     s[6, : block] = -np.inf
     _compare(s, block)
+
+
+@pytest.mark.parametrize("block", [64, 128])
+def test_row_group_path_wide_launch(block):
+    # enough rows to give every CU a 64-row workgroup: the 1024-thread form of
+    # the row-group kernel, with a ragged last workgroup
+    s = random_scores(16384 + 37, 4 * block + 4, seed=block + 11, std=6.0, masked_frac=0.02)
+    s[-1, :] = -np.inf
+    _compare(s, block)
