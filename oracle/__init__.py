@@ -82,6 +82,8 @@ def _load():
     L.orc_hif8_check_patterns.argtypes = [ctypes.c_uint64, i64, P, i32, i32, ctypes.POINTER(i64)]
     L.orc_exp2_table.restype = None
     L.orc_exp2_table.argtypes = [P, i32]
+    L.orc_power_product.restype = None
+    L.orc_power_product.argtypes = [P, i64, i32, P]
     L.orc_attention.restype = i32
     L.orc_attention.argtypes = [P, P, P, i32, i32, i32, i32, i32, i32, i32, i32,
                                 i32, i32, i32, i32, d, P, i64, P, P, P, i32]
@@ -152,6 +154,19 @@ def exp2_table(variant: int = 0) -> np.ndarray:
     variant 1: Alg. 2 with its FP16 carrier."""
     out = np.zeros(256, dtype=np.uint8)
     _load().orc_exp2_table(_ptr(out), int(variant))
+    return out
+
+
+def power_product(x, integer: bool) -> np.ndarray:
+    """Sec. 3.3 and Fig. 2: log2 of (running product of rescale factors
+    2^x_1 ... 2^x_i as the 8-bit pipeline forms them / its ground truth),
+    after every step i.  integer=True raises each exponent to an integer
+    (ceil, as Alg. 1's integer maximum does) and takes the exact power of
+    two; integer=False takes each factor as E8[Q8(x)] (an 8-bit cast of the
+    exponent, then of its power of two)."""
+    x = np.ascontiguousarray(np.asarray(x, dtype=np.float64).reshape(-1))
+    out = np.empty(x.size, dtype=np.float64)
+    _load().orc_power_product(_ptr(x), x.size, int(bool(integer)), _ptr(out))
     return out
 
 

@@ -338,6 +338,35 @@ void orc_exp2_table(uint8_t out[256], int variant)
     }
 }
 
+/* Sec. 3.3 and Fig. 2: the error that a running product of rescale factors
+ * 2^x_1 * 2^x_2 * ... picks up in the 8-bit pipeline.
+ *   integer != 0: each exponent is first raised to an integer, k = ceil(x)
+ *     (as the integer running maximum of Alg. 1 does), and the factor 2^k is
+ *     exact; the ground truth is 2^(k_1 + ... + k_i).
+ *   integer == 0 ("direct" exponents): each factor is the 8-bit pipeline's
+ *     E8[Q8(x)], the exponent cast to HiF8 and its power of two cast to HiF8;
+ *     the ground truth is 2^(x_1 + ... + x_i).
+ * out[i] = log2 of (product of the first i+1 factors / ground truth), both
+ * sides summed as log2 in fp64, so the result has no underflow at any
+ * length and is exactly 0 when every factor is exact. */
+void orc_power_product(const double* x, int64_t n, int integer, double* out)
+{
+    double lp = 0.0, lt = 0.0;
+    for (int64_t i = 0; i < n; ++i) {
+        double f, t;
+        if (integer) {
+            t = ceil(x[i]);
+            f = exp2(t);
+        } else {
+            t = x[i];
+            f = e8_hif8(orc_hif8_round(x[i], 1));
+        }
+        lp += log2(f);
+        lt += t;
+        out[i] = lp - lt;
+    }
+}
+
 /* ------------------------------------------------------------------------ */
 /* Attention                                                                 */
 /* ------------------------------------------------------------------------ */
