@@ -134,6 +134,35 @@ def softmax_setups(cfg, steps=20):
     return res
 
 
+def rescale_accumulation(delta=0.02, sks=(1024, 4096, 16384, 32768)):
+    """Sec. 3.3 / Fig. 2 on the kernels: scores that climb by `delta` log2
+    units per 128-key block (workloads.make_slow_climb; B=1, Hq=8, Hkv=2,
+    Sq=64, D=128, non-causal) move the running maximum by a small non-integer
+    step at nearly every block.  Reported: rel-L2 of O from the Exp2 HiF8
+    setup (8-bit powers of two of real-valued steps) and from E2E HiF8
+    (Alg. 1, exact integer powers) against the Default setup's fp32 softmax
+    on the same kernels (itself about 1e-6 from exact attention)."""
+    import torch
+    import paper_2602_02071_amd as baps
+    from paper_2602_02071_amd.workloads import make_slow_climb
+    dev = torch.device("cuda:0")
+    B, Hq, Hkv, Sq, D, blk = 1, 8, 2, 64, 128, 128
+    res = {"delta_log2_per_block": delta, "shape": f"B{B} Hq{Hq} Hkv{Hkv} Sq{Sq} D{D} block{blk} non-causal",
+           "Sk": list(sks), "rel_l2_vs_default": {"exp2_hif8": [], "e2e_hif8": []}}
+    for Sk in sks:
+        q, k, v = make_slow_climb(B, Hq, Hkv, Sq, Sk, D, delta, blk, seed=Sk)
+        qt, kt, vt = (torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).to(dev) for x in (q, k, v))
+        outs = {}
+        for name, mode in (("default", baps.BAPS_MODE_DEFAULT), ("exp2_hif8", baps.BAPS_MODE_EXP2_HIF8),
+                           ("e2e_hif8", baps.BAPS_MODE_E2E_HIF8)):
+            outs[name], _ = baps.attention(qt, kt, vt, False, blk, mode=mode)
+        torch.cuda.synchronize()
+        ref = outs["default"].double()
+        for name in ("exp2_hif8", "e2e_hif8"):
+            res["rel_l2_vs_default"][name].append(float((outs[name].double() - ref).norm() / ref.norm()))
+    return res
+
+
 def fp8_qk(steps=20):
     """FP8 E4M3 Q/K (per-tensor scales) against bf16 on the same workloads:
     the Llama-3-8B prefill (QK^T on the FP8 matrix cores: the dense peak of
@@ -372,6 +401,7 @@ def main():
     ap.add_argument("--no-modes", action="store_true", help="skip the Default / Exp2 HiF8 comparison")
     ap.add_argument("--no-restart-rates", action="store_true", help="skip the tile restart-rate table")
     ap.add_argument("--no-fp8", action="store_true", help="skip the FP8 Q/K comparison")
+    ap.add_argument("--no-accumulation", action="store_true", help="skip the rescale-accumulation error table")
     ap.add_argument("--no-other", action="store_true", help="skip the ViT and long-prefill workloads")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run a plain device copy of this many MiB (counter calibration)")
@@ -418,6 +448,8 @@ def main():
                                       "frac": gbs / PEAK_HBM_GBS, "traffic": _traffic("attn_fwd_decode")}}
     if not args.no_modes and w.Sq > 1:
         out["softmax_setups"] = softmax_setups(args.config)
+    if not args.no_accumulation:
+        out["rescale_accumulation"] = rescale_accumulation()
     if not args.no_restart_rates:
         out["restart_rates"] = restart_rates()
     if not args.no_fp8:

@@ -109,6 +109,22 @@ def make_qkv(B, Hq, Hkv, Sq, Sk, D, seed=0, outliers=False, sink=0, lognormal_k=
     return f32_to_bf16_bits(q), f32_to_bf16_bits(k), f32_to_bf16_bits(v)
 
 
+def make_slow_climb(B, Hq, Hkv, Sq, Sk, D, delta, block, seed=0):
+    """bf16 q [B,Hq,Sq,D], k, v [B,Hkv,Sk,D] whose scores climb slowly along
+    the keys: every query is close to the all-ones vector and key t carries
+    the offset t * delta / (block * sqrt(D) * log2(e)) in every channel, so
+    the score in log2 units (scale 1/sqrt(D)) rises by about `delta` per key
+    block.  The running maximum then moves by a small non-integer step at
+    nearly every block while the early blocks keep their weight: the case
+    where the rescale factors of the online softmax compound.  Small noise
+    (seed+1000 for Q, seed+2000 for K, seed+3000 for V) keeps rows distinct."""
+    q = np.float32(1.0) + np.float32(0.01) * _normal(seed + 1000, (B, Hq, Sq, D))
+    ramp = (np.arange(Sk, dtype=np.float64) * delta / (block * math.sqrt(D) * math.log2(math.e))).astype(np.float32)
+    k = ramp[None, None, :, None] + np.float32(0.01) * _normal(seed + 2000, (B, Hkv, Sk, D))
+    v = _normal(seed + 3000, (B, Hkv, Sk, D))
+    return f32_to_bf16_bits(q), f32_to_bf16_bits(k), f32_to_bf16_bits(v)
+
+
 def quantize_e4m3(x: np.ndarray, scale: float) -> np.ndarray:
     """OCP FP8 E4M3 codes of x / scale: round to nearest, ties to even,
     saturating at +-448 (the inputs of the FP8 Q/K path)."""

@@ -49,3 +49,27 @@ def test_mode_llama_prefill_sampled_rows(mode):
     shape = (w.B, w.Hq, w.Hkv, w.Sq, w.Sk, w.D, w.causal)
     rows = sample_rows(w, every=512, tile=1024, heads=range(0, w.Hq, 5))
     _check(q, k, v, shape, w.block, MODES[mode], rows=rows, label=f"{mode} {w.name}")
+
+
+def test_accumulated_rescale_error_grows_only_with_direct_powers():
+    """Sec. 3.3 / Fig. 2 on the kernels: scores that climb by 0.02 log2 units
+    per key block move the running maximum by a small non-integer step at
+    almost every block.  Exp2 HiF8 multiplies its accumulators by an 8-bit
+    power of two of that step, which rounds to 1, and the drift compounds
+    with the number of blocks; Alg. 1's integer maximum rescales by exact
+    powers of two and stays at the error of its 8-bit P.  Both kernels match
+    the oracle on these inputs; the errors are against exact attention."""
+    from paper_2602_02071_amd.workloads import make_slow_climb
+    err = {}
+    for Sk in (2048, 16384):
+        shape = (1, 4, 1, 16, Sk, 128, False)
+        B, Hq, Hkv, Sq, _, D, causal = shape
+        q, k, v = make_slow_climb(B, Hq, Hkv, Sq, Sk, D, 0.02, 128, seed=Sk)
+        exact, _ = O.exact_attention(q, k, v, B, Hq, Hkv, Sq, Sk, D, causal)
+        for name, mode in (("e2e", O.E2E_HIF8), ("exp2", O.EXP2_HIF8)):
+            o, lse = gpu_attention(q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, 128, mode=mode)
+            check_parity(q, k, v, shape, 128, o, lse, label=f"slow climb {name} Sk={Sk}", mode=mode)
+            err[name, Sk] = float(np.linalg.norm(o - exact) / np.linalg.norm(exact))
+    assert err["e2e", 16384] < 0.06, err
+    assert err["exp2", 16384] > 2 * err["exp2", 2048], err
+    assert err["exp2", 16384] > 4 * err["e2e", 16384], err
