@@ -18,6 +18,10 @@ using namespace baps;
 __device__ uint32_t g_score_table[kTabEntries];
 // The compact code table of the fused attention kernels (see common.hpp).
 __device__ __attribute__((aligned(256))) uint8_t g_code_table[kCodeTableBytes];
+// The same table expanded to every score-table index (indices below kCodeLo
+// take the entry of kCodeLo, above kCodeHi that of kCodeHi), so that a lookup
+// needs no clamp; the prefill kernel copies it into LDS as it is.
+__device__ __attribute__((aligned(1024))) uint8_t g_code_table_x[kTabEntries];
 
 // HiF8 value of a double, rounded once: truncating to fp32 toward zero keeps
 // the sign, the exponent and the leading mantissa bits that decide a
@@ -59,6 +63,7 @@ uint8_t linear_code(float p)
 struct Table {
     uint32_t e[kTabEntries];
     uint8_t code[kCodeEntries];
+    uint8_t codex[kTabEntries];
     Table()
     {
         for (uint32_t i = 0; i < (uint32_t)kTabEntries; ++i) {
@@ -68,6 +73,7 @@ struct Table {
             e[i] = (pb & 0xffffff00u) | hif8::encode(p, true);
         }
         for (int i = 0; i < kCodeEntries; ++i) code[i] = linear_code(hif8::u2f(e[kCodeLo + i] & 0xffffff00u));
+        for (int i = 0; i < kTabEntries; ++i) codex[i] = code[(i < kCodeLo ? kCodeLo : (i > kCodeHi ? kCodeHi : i)) - kCodeLo];
     }
 };
 
@@ -81,6 +87,7 @@ constexpr int kMaxDevices = 64;
 std::mutex g_mutex;
 const uint32_t* g_dev_table[kMaxDevices] = {};
 const uint8_t* g_dev_code[kMaxDevices] = {};
+const uint8_t* g_dev_codex[kMaxDevices] = {};
 
 // the last HIP failure a call of this library met on the calling thread
 thread_local hipError_t g_last_hip = hipSuccess;
@@ -97,7 +104,7 @@ int status_of(hipError_t e)
 // their launches, so it is cleared first: a launch is judged on its own.
 void clear_stale_error() { (void)hipGetLastError(); }
 
-int table_on_current_device(const uint32_t** out, const uint8_t** code = nullptr)
+int table_on_current_device(const uint32_t** out, const uint8_t** code = nullptr, const uint8_t** codex = nullptr)
 {
     int dev = 0;
     if (int st = status_of(hipGetDevice(&dev))) return st;
@@ -115,12 +122,19 @@ int table_on_current_device(const uint32_t** out, const uint8_t** code = nullptr
             return st;
         void* cptr = nullptr;
         if (int st = status_of(hipGetSymbolAddress(&cptr, HIP_SYMBOL(g_code_table)))) return st;
-        if (!ptr || !cptr) return BAPS_HIP_ERROR;
+        if (int st = status_of(hipMemcpyToSymbol(HIP_SYMBOL(g_code_table_x), t.codex, sizeof(t.codex), 0,
+                                                 hipMemcpyHostToDevice)))
+            return st;
+        void* xptr = nullptr;
+        if (int st = status_of(hipGetSymbolAddress(&xptr, HIP_SYMBOL(g_code_table_x)))) return st;
+        if (!ptr || !cptr || !xptr) return BAPS_HIP_ERROR;
         g_dev_code[dev] = static_cast<const uint8_t*>(cptr);
+        g_dev_codex[dev] = static_cast<const uint8_t*>(xptr);
         g_dev_table[dev] = static_cast<const uint32_t*>(ptr);
     }
     *out = g_dev_table[dev];
     if (code) *code = g_dev_code[dev];
+    if (codex) *codex = g_dev_codex[dev];
     return BAPS_OK;
 }
 
@@ -188,6 +202,7 @@ int make_params(const void* q, const void* k, const void* v, float* o, float* ls
     AttnParams& p = *out;
     p.tab = nullptr;
     p.ctab = nullptr;
+    p.ctabx = nullptr;
     p.q = static_cast<const uint16_t*>(q);
     p.k = static_cast<const uint16_t*>(k);
     p.v = static_cast<const uint16_t*>(v);
@@ -215,9 +230,11 @@ int attach_tables(AttnParams* p)
 {
     const uint32_t* tab = nullptr;
     const uint8_t* ctab = nullptr;
-    const int st = table_on_current_device(&tab, &ctab);
+    const uint8_t* ctabx = nullptr;
+    const int st = table_on_current_device(&tab, &ctab, &ctabx);
     p->tab = tab;
     p->ctab = ctab;
+    p->ctabx = ctabx;
     return st;
 }
 

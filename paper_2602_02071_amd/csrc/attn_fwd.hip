@@ -194,7 +194,102 @@ __device__ __forceinline__ void load_tile_k8(const uint8_t* base, int key0, int 
     }
 }
 
-template <int D, int BLK, int NW, bool CT, int MODE, bool TILE, bool F8>
+// Work items are (query tile, key/value head, batch) triples with a linear
+// id L.  When the (batch, key/value head) count is a multiple of 8, L % 8 is
+// the head class: workgroups are dealt to the 8 XCDs round-robin by id, each
+// XCD with its own L2, and the schedule below keeps every item of a class on
+// the workgroups of one XCD, so that a head's K/V is fetched into one L2
+// only.  Otherwise L runs over the tiles of all heads.  Either way the
+// longest causal tiles come first.
+__device__ __forceinline__ void decode_item(int L, int ntiles, int heads, int Hkv, int& tile, int& g, int& b)
+{
+    int t_rev, hk;
+    if (heads % 8 == 0) {
+        const int hpx = heads / 8;                      // heads per class
+        const int k = L >> 3;
+        hk = (L & 7) + 8 * (k % hpx);
+        t_rev = k / hpx;
+    } else {
+        t_rev = L / heads;
+        hk = L % heads;
+    }
+    tile = ntiles - 1 - t_rev;
+    g = hk % Hkv;
+    b = hk / Hkv;
+}
+
+// The persistent schedule: nwg resident workgroups share nitems items.  With
+// nwg a multiple of 8, workgroup w serves class w % 8 alone: in round r it
+// takes item r*nwg/8 + k of the class (k = w / 8) on even rounds and
+// r*nwg/8 + nwg/8 - 1 - k on odd rounds.  Items come longest first, so the
+// back-and-forth order pairs long tiles with short ones (a causal workload
+// with two items per workgroup gets the same number of key blocks on every
+// workgroup).  Returns -1 past the last item.
+__device__ __forceinline__ int item_at(int r, int w, int nwg, int nitems)
+{
+    if (nwg >= nitems) return r == 0 ? w : -1;
+    int L;
+    if (nwg % 8 == 0) {
+        const int g8 = nwg >> 3, k = w >> 3;
+        L = 8 * (r * g8 + ((r & 1) ? g8 - 1 - k : k)) + (w & 7);
+    } else {
+        L = r * nwg + ((r & 1) ? nwg - 1 - w : w);
+    }
+    return L < nitems ? L : -1;
+}
+
+// A value the compiler must take as new at this point (keeps computations
+// derived from it where they are written)
+__device__ __forceinline__ void opaque_v(int& x) { asm volatile("" : "+v"(x)); }
+__device__ __forceinline__ void opaque_s(int& x) { asm volatile("" : "+s"(x)); }
+
+typedef __attribute__((address_space(4))) const AttnParams* kargs_ptr;
+
+// The kernel's arguments through a pointer the compiler cannot see through:
+// loads from it stay where they are written (once per work item) instead of
+// holding those fields in scalar registers across the key-block loop.
+__device__ __forceinline__ kargs_ptr fresh_args()
+{
+    kargs_ptr a = (kargs_ptr)__builtin_amdgcn_kernarg_segment_ptr();
+    asm volatile("" : "+s"(a));
+    return a;
+}
+
+// An item's tile, key/value head, batch and key blocks (its last row sees
+// the most keys).
+struct ItemGeo {
+    int tile, g, b, nblk;
+};
+
+template <int BLK, int TILE_ROWS>
+__device__ __forceinline__ ItemGeo item_geo(int L, int Hq, int Hkv, int B, int Sq, int Sk, int causal)
+{
+    const int G = Hq / Hkv;
+    const int flat_rows = Sq * G;
+    const int ntiles = (flat_rows + TILE_ROWS - 1) / TILE_ROWS;
+    ItemGeo e;
+    decode_item(L, ntiles, B * Hkv, Hkv, e.tile, e.g, e.b);
+    const int f_last = min(flat_rows - 1, e.tile * TILE_ROWS + TILE_ROWS - 1);
+    const int kmax_tile = causal ? min(Sk - 1, f_last / G + Sk - Sq) : Sk - 1;
+    e.nblk = kmax_tile < 0 ? 0 : kmax_tile / BLK + 1;
+    return e;
+}
+
+// The item a workgroup takes in round r, with its geometry; false past the last
+template <int BLK, int TILE_ROWS>
+__device__ __forceinline__ bool item_of_round(kargs_ptr a, int r, ItemGeo& e)
+{
+    const int ntiles = (a->Sq * (a->Hq / a->Hkv) + TILE_ROWS - 1) / TILE_ROWS;
+    const int L = item_at(r, blockIdx.x, gridDim.x, ntiles * a->B * a->Hkv);
+    if (L < 0) return false;
+    e = item_geo<BLK, TILE_ROWS>(L, a->Hq, a->Hkv, a->B, a->Sq, a->Sk, a->causal);
+    return true;
+}
+
+// PERSIST: the grid holds at most as many workgroups as the GPU runs at once
+// and each takes a sequence of items (item_at); otherwise one item per
+// workgroup.
+template <int D, int BLK, int NW, bool CT, int MODE, bool TILE, bool F8, bool PERSIST>
 __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
 {
     static_assert(MODE == kModeE2E || CT, "the eq. (2) setups use the compact table (T <= 0)");
@@ -202,10 +297,10 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
     static_assert(D == 64 || D == 128, "head dimension");
     static_assert(BLK % 32 == 0 && BLK <= 128, "key block");
     using C = Cfg<D, BLK, NW>;
-    // P lookup: the code table (lambda <= kCodeMaxLambda) expanded to all
-    // 8192 indices, so that a lookup needs no clamp; else the bf16 half of the
-    // full score table
-    __shared__ __attribute__((aligned(16))) uint8_t ctab[CT ? kTabEntries : 1];
+    // P lookup: with the code table (lambda <= kCodeMaxLambda) the table
+    // expanded to all 8192 indices (no lookup needs a clamp); else the bf16
+    // half of the full score table
+    __shared__ __attribute__((aligned(1024))) uint8_t ctab[CT ? kTabEntries : 1];
     __shared__ __attribute__((aligned(16))) uint16_t tab[CT ? 1 : kTabEntries];
     __shared__ uint32_t tflag[TILE ? NW : 1][3];  // per wave: rows that restart, see the block, are in B0
     extern __shared__ __attribute__((aligned(1024))) char tiles[];
@@ -214,80 +309,20 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
     constexpr int kKT = BLK / 32;                 // 32-key tiles per block
     constexpr int kDK = D / 16;                   // 16-wide d chunks (QK^T contraction)
     constexpr int kDT = D / 32;                   // 32-wide d tiles of O^T
+    constexpr int kDK8 = D / 64;                  // 64-wide d chunks (FP8 QK^T)
 
+    static_assert((NW & (NW - 1)) == 0, "waves per workgroup");
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    // (the mask states the bound wave < NW, which folds the per-wave load
+    // counts of the K/V tiles to constants)
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6) & (NW - 1);
     const int j32 = lane & 31;
     const int half = lane >> 5;
 
     const int G = p.Hq / p.Hkv;
     const int flat_rows = p.Sq * G;
-    const int ntiles = (flat_rows + C::kTileRows - 1) / C::kTileRows;
-    // Work item (tile, key/value head, batch).  Workgroups are dealt to the 8
-    // XCDs round-robin by linear id, each XCD with its own L2; when the
-    // (batch, kv head) count is a multiple of 8, the linear id L is mapped so
-    // that every tile of a kv head runs on the same XCD (L % 8 picks the head
-    // class) and its K/V is fetched into one L2 only.  Within an XCD the
-    // longest causal tiles go first.
-    int tile, g, b;
-    {
-        const int L = (int)(blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z));
-        const int heads = p.B * p.Hkv;
-        int t_rev, hk;
-        if (heads % 8 == 0) {
-            const int hpx = heads / 8;                      // heads per XCD
-            const int k = L >> 3;
-            hk = (L & 7) + 8 * (k % hpx);
-            t_rev = k / hpx;
-        } else {
-            t_rev = L % ntiles;
-            hk = L / ntiles;
-        }
-        tile = ntiles - 1 - t_rev;
-        g = hk % p.Hkv;
-        b = hk / p.Hkv;
-    }
-    const uint16_t* kbase = p.k + ((long long)b * p.Hkv + g) * (long long)p.Sk * D;
-    const uint8_t* kbase8 = reinterpret_cast<const uint8_t*>(p.k) + ((long long)b * p.Hkv + g) * (long long)p.Sk * D;
-    const uint16_t* vbase = p.v + ((long long)b * p.Hkv + g) * (long long)p.Sk * D;
-
-    // key extent of the workgroup: its last row sees the most keys
     const int off = p.Sk - p.Sq;                            // bottom-right causal alignment
-    const int f_last = min(flat_rows - 1, tile * C::kTileRows + C::kTileRows - 1);
-    const int kmax_tile = p.causal ? min(p.Sk - 1, f_last / G + off) : p.Sk - 1;
-    const int nblk = kmax_tile < 0 ? 0 : kmax_tile / BLK + 1;
-
-    if (nblk > 0) {
-        if constexpr (F8) load_tile_k8<D, BLK, NW>(kbase8, 0, p.Sk, tiles_lds, wave, lane);
-        else load_tile<D, BLK, NW, false>(kbase, 0, p.Sk, tiles_lds, wave, lane);
-        load_tile<D, BLK, NW, true>(vbase, 0, p.Sk, tiles_lds + C::kTileBytes, wave, lane);
-    }
-    if constexpr (MODE == kModeDefault) {
-        // fp32 exp2: no table
-    } else if constexpr (CT) {
-        // indices below kCodeLo take the entry of kCodeLo (P = 1), above
-        // kCodeHi that of kCodeHi (P = 0)
-        for (int i = tid; i < kTabEntries; i += C::kThreads) ctab[i] = p.ctab[min(max(i, kCodeLo), kCodeHi) - kCodeLo];
-    } else {
-        for (int i = tid; i < kTabEntries; i += C::kThreads) tab[i] = (uint16_t)(p.tab[i] >> 16);
-    }
-
-    // this lane's query row: flat index f = r * G + h_local
-    const int f = tile * C::kTileRows + wave * kRowsPerWave + j32;
-    const bool row_ok = f < flat_rows;
-    const int r = row_ok ? f / G : 0;
-    const int h = g * G + (row_ok ? f % G : 0);
-    const int kmax = row_ok ? (p.causal ? min(p.Sk - 1, r + off) : p.Sk - 1) : -1;
-    int kmax_wave_hi = kmax, kmax_wave_lo = row_ok ? kmax : 0x7fffffff;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        kmax_wave_hi = max(kmax_wave_hi, __shfl_xor(kmax_wave_hi, o, 64));
-        kmax_wave_lo = min(kmax_wave_lo, __shfl_xor(kmax_wave_lo, o, 64));
-    }
-    // wave-uniform from here on: keeps the skip and mask branches scalar
-    kmax_wave_hi = __builtin_amdgcn_readfirstlane(kmax_wave_hi);
-    kmax_wave_lo = __builtin_amdgcn_readfirstlane(kmax_wave_lo);
 
     // Tile-level restart (the paper's granularity, Sec. 3.2): the rows of one
     // head at restart_rows consecutive query positions share each block's
@@ -315,45 +350,6 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
             trep = half == 0 && wave == tw0 && j32 < G;
         }
     }
-
-    // Q^T as the B operand of S^T = K Q^T: lane holds Q[row][16*kk + 8*half .. +8]
-    // (FP8: 32 bytes Q[row][64*kk + 32*half .. +32] per 32x32x64 MFMA)
-    constexpr int kDK8 = D / 64;
-    u32x4 qop[F8 ? 1 : kDK];
-    i32x8 qop8[F8 ? kDK8 : 1];
-    if constexpr (F8) {
-        const uint8_t* qrow = reinterpret_cast<const uint8_t*>(p.q) + (((long long)b * p.Hq + h) * p.Sq + r) * D;
-#pragma unroll
-        for (int kk = 0; kk < kDK8; ++kk) {
-            const u32x4 lo = row_ok ? *reinterpret_cast<const u32x4*>(qrow + 64 * kk + 32 * half) : u32x4{0, 0, 0, 0};
-            const u32x4 hi = row_ok ? *reinterpret_cast<const u32x4*>(qrow + 64 * kk + 32 * half + 16) : u32x4{0, 0, 0, 0};
-            qop8[kk] = cat8(lo, hi);
-        }
-    } else {
-        const uint16_t* qrow = p.q + (((long long)b * p.Hq + h) * p.Sq + r) * D;
-#pragma unroll
-        for (int kk = 0; kk < kDK; ++kk)
-            qop[kk] = row_ok ? *reinterpret_cast<const u32x4*>(qrow + kk * 16 + half * 8) : u32x4{0, 0, 0, 0};
-    }
-
-    const float ninf = -__builtin_huge_valf();
-    const float c = p.c;
-    const float lam = (float)p.lambda;
-    // Alg. 1 state of this lane's row.  The output and the denominator are
-    // kept relative to the current block reference ref_j instead of the
-    // running maximum m_j: X_j = sum_{i<=j} 2^(ref_i - ref_j) P_i V_i and
-    // dX_j likewise, so O~_j = 2^(ref_j - m_j) X_j and d_j = 2^(ref_j - m_j) dX_j.
-    // The two power-of-two rescales of a block (2^(m_{j-1}-m_j) on the old
-    // state, 2^(ref_j - m_j) on the new block) fold into one exact rescale by
-    // 2^(ref_{j-1} - ref_j), needed only when the reference moves, and the
-    // normalisation O = O~/d = X/dX is unchanged.
-    float m = ninf;                 // running integer maximum m_j
-    float ref = ninf;               // current block reference
-    float dl = 0.0f;                // this lane's share of dX
-    unsigned n_restart = 0, n_visit = 0;
-    f32x16 oacc[kDT];
-#pragma unroll
-    for (int t = 0; t < kDT; ++t) oacc[t] = f32x16{};
 
     // per-lane LDS byte offsets of the operand reads inside a tile
     uint32_t koff[F8 ? 2 * kDK8 : kDK];
@@ -390,285 +386,404 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
         }
     }
 
-    for (int jb = 0; jb < nblk; ++jb) {
-        const int key0 = jb * BLK;
-        const char* kt_lds = tiles + (jb & 1) * 2 * C::kTileBytes;
-        const char* vt_lds = kt_lds + C::kTileBytes;
-        __builtin_amdgcn_s_waitcnt(0);                      // this wave's loads of block jb landed
-        __syncthreads();                                    // everyone's did; block jb-1 fully consumed
-        if (jb + 1 < nblk) {
-            const uint32_t nk = tiles_lds + ((jb + 1) & 1) * 2 * C::kTileBytes;
-            const int k1 = key0 + BLK;
-            if (k1 + BLK <= p.Sk) {                         // the whole next block lies before Sk
-                if constexpr (F8) load_tile_sb<kNJK, NW, kLoadsK>(kbase8 + (long long)k1 * D, kdofs, nk, wave);
-                else load_tile_sb<kNJK, NW, kLoadsK>(kbase + (long long)k1 * D, kdofs, nk, wave);
-                load_tile_sb<kNJV, NW, C::kLoadsPerTile>(vbase + (long long)k1 * D, vdofs, nk + C::kTileBytes, wave);
-            } else {
-                if constexpr (F8) load_tile_k8<D, BLK, NW>(kbase8, k1, p.Sk, nk, wave, lane);
-                else load_tile<D, BLK, NW, false>(kbase, k1, p.Sk, nk, wave, lane);
-                load_tile<D, BLK, NW, true>(vbase, k1, p.Sk, nk + C::kTileBytes, wave, lane);
-            }
+    // key/value head offset (elements; bytes for FP8 K) of an item
+    auto kv_off = [&](const ItemGeo& e) { return ((long long)e.b * p.Hkv + e.g) * (long long)p.Sk * D; };
+    // Asynchronous loads of key block jb of the key/value head at hoff into K/V buffer sel
+    auto issue_block = [&](long long hoff, int jb, int sel) {
+        const uint8_t* kb8 = reinterpret_cast<const uint8_t*>(p.k) + hoff;
+        const uint16_t* kb = p.k + hoff;
+        const uint16_t* vb = p.v + hoff;
+        const uint32_t nk = tiles_lds + sel * 2 * C::kTileBytes;
+        const int k1 = jb * BLK;
+        if (k1 + BLK <= p.Sk) {                             // the whole block lies before Sk
+            if constexpr (F8) load_tile_sb<kNJK, NW, kLoadsK>(kb8 + (long long)k1 * D, kdofs, nk, wave);
+            else load_tile_sb<kNJK, NW, kLoadsK>(kb + (long long)k1 * D, kdofs, nk, wave);
+            load_tile_sb<kNJV, NW, C::kLoadsPerTile>(vb + (long long)k1 * D, vdofs, nk + C::kTileBytes, wave);
+        } else {
+            if constexpr (F8) load_tile_k8<D, BLK, NW>(kb8, k1, p.Sk, nk, wave, lane);
+            else load_tile<D, BLK, NW, false>(kb, k1, p.Sk, nk, wave, lane);
+            load_tile<D, BLK, NW, true>(vb, k1, p.Sk, nk + C::kTileBytes, wave, lane);
         }
-        // A wave that sees nothing of the block skips it.  In a tile that
-        // spans waves it still takes part in the tile's exchange below, with
-        // no visible row (its row maximum stays -inf): the exchange has one
-        // barrier on one path, and the tile's representative lane counts the
-        // block whenever any row of the tile sees it.
-        const bool live = key0 <= kmax_wave_hi;
-        if (!live && !(TILE && xwave)) continue;
+    };
 
-        f32x16 sacc[kKT];
-#pragma unroll
-        for (int kt = 0; kt < kKT; ++kt) sacc[kt] = f32x16{};
-        float amax = ninf;
-        if (live) {
-        // S^T = K_j Q^T.  The wave raises its priority for the MFMA burst so
-        // that the two waves sharing a SIMD drift apart: one runs its QK^T
-        // MFMAs while the other runs the VALU softmax of its block.
-        __builtin_amdgcn_s_setprio(2);
+    // Q^T as the B operand of S^T = K Q^T: lane holds Q[row][16*kk + 8*half .. +8]
+    // (FP8: 32 bytes Q[row][64*kk + 32*half .. +32] per 32x32x64 MFMA)
+    u32x4 qop[F8 ? 1 : kDK];
+    i32x8 qop8[F8 ? kDK8 : 1];
+    auto load_q = [&](kargs_ptr a, const ItemGeo& e) {
+        int ln = lane, Gi = G;
+        opaque_v(ln);
+        opaque_s(Gi);
+        const int hf = ln >> 5;
+        const int f = e.tile * C::kTileRows + wave * kRowsPerWave + (ln & 31);
+        const bool ok = f < flat_rows;
+        const int r = ok ? f / Gi : 0;
+        const int h = e.g * Gi + (ok ? f % Gi : 0);
         if constexpr (F8) {
-            // FP8 E4M3 on both sides, unit block scales (E8M0 127): the
-            // dequantisation scales are folded into c
+            const uint8_t* qrow = reinterpret_cast<const uint8_t*>(a->q) + (((long long)e.b * a->Hq + h) * a->Sq + r) * D;
 #pragma unroll
             for (int kk = 0; kk < kDK8; ++kk) {
-#pragma unroll
-                for (int kt = 0; kt < kKT; ++kt) {
-                    const char* kp = kt_lds + kt * 32 * D;
-                    const u32x4 lo = *reinterpret_cast<const u32x4*>(kp + koff[2 * kk]);
-                    const u32x4 hi = *reinterpret_cast<const u32x4*>(kp + koff[2 * kk + 1]);
-                    sacc[kt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(cat8(lo, hi), qop8[kk], sacc[kt],
-                                                                               0, 0, 0, 127, 0, 127);
-                }
+                const u32x4 lo = ok ? *reinterpret_cast<const u32x4*>(qrow + 64 * kk + 32 * hf) : u32x4{0, 0, 0, 0};
+                const u32x4 hi = ok ? *reinterpret_cast<const u32x4*>(qrow + 64 * kk + 32 * hf + 16) : u32x4{0, 0, 0, 0};
+                qop8[kk] = cat8(lo, hi);
             }
         } else {
-            __builtin_amdgcn_sched_barrier(0);
+            const uint16_t* qrow = a->q + (((long long)e.b * a->Hq + h) * a->Sq + r) * D;
 #pragma unroll
-            for (int kk = 0; kk < kDK; ++kk) {
-                const char* kp = kt_lds + koff[kk];
-#pragma unroll
-                for (int kt = 0; kt < kKT; ++kt) {
-                    const u32x4 a = *reinterpret_cast<const u32x4*>(kp + kt * 32 * C::kRowBytes);
-                    sacc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(qop[kk]), sacc[kt],
-                                                                       0, 0, 0);
-                }
-            }
-            // keep kKReads operand reads in flight ahead of the MFMAs that
-            // consume them (the default schedule keeps two, and the MFMAs
-            // wait on LDS latency)
-            constexpr int kKReads = 4;
-            __builtin_amdgcn_sched_group_barrier(0x100, kKReads, 0);          // LDS reads
-#pragma unroll
-            for (int i = 0; i < kDK * kKT - kKReads; ++i) {
-                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);            // one MFMA
-                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);            // one LDS read
-            }
-            __builtin_amdgcn_sched_group_barrier(0x008, kKReads, 0);
-            __builtin_amdgcn_sched_barrier(0);
+            for (int kk = 0; kk < kDK; ++kk)
+                qop[kk] = ok ? *reinterpret_cast<const u32x4*>(qrow + kk * 16 + hf * 8) : u32x4{0, 0, 0, 0};
         }
-        __builtin_amdgcn_s_setprio(0);
-        // mask keys past kmax (causal diagonal, ragged tail); key of register
-        // i of tile kt: key0 + 32*kt + 8*(i/4) + 4*half + i%4
-        if (key0 + BLK - 1 > kmax_wave_lo) {
-            asm volatile("" ::: "memory");          // keep this a real branch (no if-conversion)
-            const int lim = kmax - key0 - 4 * half;
-#pragma unroll
-            for (int kt = 0; kt < kKT; ++kt)
-#pragma unroll
-                for (int i = 0; i < 16; ++i)
-                    if (kt * 32 + 8 * (i / 4) + (i % 4) > lim) sacc[kt][i] = ninf;
-        }
-        // row maximum of the raw dot products (the scale c > 0 is monotone):
-        // a 3-way tree over this lane's 16*kKT scores, then lanes l and l^32
-        {
-            float mx[16 * kKT];
-#pragma unroll
-            for (int kt = 0; kt < kKT; ++kt)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) mx[16 * kt + i] = sacc[kt][i];
-            amax = tree_max<16 * kKT>(mx);
-            amax = __builtin_fmaxf(amax, swap_halves(amax));
-        }
-        }  // live
+    };
 
-        float nref;
-        if constexpr (MODE == kModeE2E) {
-            // block-aware precision rescaling (Alg. 1), per row, branch-free.
-            // B0 blocks (and a first block with m = -inf) take the high-precision
-            // path; B1 blocks restart when ceil(rowmax T) > lambda, where rowmax of
-            // the 8-bit T = fl32(acc*c - m) is the 8-bit cast of the raw maximum's
-            // T (the cast is monotone).
-            const bool vis = (!TILE || row_ok) && amax != ninf;
-            const bool in_b0 = (jb < p.n_b0) || (p.b0_last && jb == kmax / BLK);
-            const bool forced = in_b0 || (m == ninf);
-            const float tq = hif8::round(__builtin_fmaf(amax, c, -m));
-            bool restart = forced || (ceilf(tq) > lam);
-            if constexpr (TILE) {
-                // the tile restarts when any of its rows that see the block would
-                const uint32_t wantb = (uint32_t)__ballot(vis && restart);
-                const uint32_t visb = (uint32_t)__ballot(vis);
-                const uint32_t b0b = (uint32_t)__ballot(vis && in_b0);
-                uint32_t tw, tv, tb;
-                if (!xwave) {
-                    tw = wantb & tmask;
-                    tv = visb & tmask;
-                    tb = b0b & tmask;
-                } else {
-                    if (lane == 0) {
-                        tflag[wave][0] = wantb;
-                        tflag[wave][1] = visb;
-                        tflag[wave][2] = b0b;
-                    }
-                    __syncthreads();
-                    uint32_t a = 0, vv = 0, z = 0;
-                    for (int w = tw0; w < tw0 + twn; ++w) {
-                        a |= tflag[w][0];
-                        vv |= tflag[w][1];
-                        z |= tflag[w][2];
-                    }
-                    tw = a & tmask;
-                    tv = vv & tmask;
-                    tb = z & tmask;
-                }
-                restart = tw != 0u;
-                if (trep && tv && !tb) {                    // a B1 tile-block
-                    ++n_visit;
-                    n_restart += restart ? 1u : 0u;
-                }
-            } else {
-                const bool b1 = vis && !in_b0;
-                n_visit += b1 ? 1u : 0u;
-                n_restart += (b1 && restart) ? 1u : 0u;
-            }
-            const float m_hi = __builtin_fmaxf(m, ceilf(amax * c));    // ceil(rowmax S), S in fp32
-            const float m_new = vis ? (restart ? m_hi : m + __builtin_fmaxf(0.0f, ceilf(tq))) : m;
-            const float ref_new = vis ? (restart ? m_hi : m) : ref;
-            const float f = (ref == ninf) ? 1.0f : exp2_int(ref - ref_new);
-            if (__any(f != 1.0f)) {
-    #pragma unroll
-                for (int t = 0; t < kDT; ++t)
-    #pragma unroll
-                    for (int i = 0; i < 16; ++i) oacc[t][i] *= f;
-            }
-            dl *= f;
-            m = m_new;
-            ref = ref_new;
-
-            // a row with no visible key so far keeps ref = -inf; its masked scores
-            // (acc = -inf) must still give T = -inf and P = 0
-            nref = (ref == ninf) ? 0.0f : -ref;
+    ItemGeo cur;
+    if (!item_of_round<BLK, C::kTileRows>(fresh_args(), 0, cur)) return;   // (the grid holds at most one workgroup per item)
+    if (cur.nblk > 0) issue_block(kv_off(cur), 0, 0);
+    if constexpr (MODE != kModeDefault) {                  // (Default evaluates exp2 in fp32: no table)
+        if constexpr (CT) {
+            // asynchronous copy (the LDS address handed to the loads is the
+            // table's: the compiler sees it written)
+            const uint32_t ct_lds = (uint32_t)(uintptr_t)LDS_PTR(uint8_t, ctab);
+            for (int i = wave; i < kTabEntries / 1024; i += NW)
+                lds_dma_16(p.ctabx + i * 1024 + 16 * lane, __builtin_amdgcn_readfirstlane(ct_lds + i * 1024));
         } else {
-            // eq. (2): real-valued running maximum m, rescale factor
-            // 2^(m_old - m) in fp32 (Default) or HiF8(2^HiF8(m_old - m)) (Exp2 HiF8)
-            const bool vis = amax != ninf;
-            const float m_new = vis ? __builtin_fmaxf(m, amax * c) : m;   // fl32(max acc * c) = max S
-            float f = 1.0f;
-            if (m != ninf) {
-                const float x = m - m_new;
-                if constexpr (MODE == kModeDefault) {
-                    f = __builtin_amdgcn_exp2f(x);
-                } else {
-                    f = hif8::u2f((uint32_t)ctab[hif8::f2u(x) >> kTabShift] << 20) * 0x1p104f;
-                }
-            }
-            if (__any(f != 1.0f)) {
-#pragma unroll
-                for (int t = 0; t < kDT; ++t)
-#pragma unroll
-                    for (int i = 0; i < 16; ++i) oacc[t][i] *= f;
-            }
-            dl *= f;
-            m = m_new;
-            ref = m_new;
-            nref = (m == ninf) ? 0.0f : -m;
-        }
-
-        if (!live) continue;
-        const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
-#pragma unroll
-        for (int kt = 0; kt < kKT; ++kt) {
-            // P = HiF8(2^HiF8(T)), T = fl32(acc*c - ref), for this 32-key tile,
-            // packed as two bf16 B operands
-            u32x4 pop[2];
-#pragma unroll
-            for (int ch = 0; ch < 2; ++ch) {
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    uint32_t w;
-                    if constexpr (MODE == kModeDefault) {
-                        // P = 2^fl32(S - m) in fp32; bf16 into P V, fp32 into the sum
-                        const float p0 = __builtin_amdgcn_exp2f(sacc[kt][ch * 8 + 2 * e] * c + nref);
-                        const float p1 = __builtin_amdgcn_exp2f(sacc[kt][ch * 8 + 2 * e + 1] * c + nref);
-                        const bf16x2 pb = {(__bf16)p0, (__bf16)p1};
-                        w = __builtin_bit_cast(uint32_t, pb);
-                        dl += p0 + p1;
-                        pop[ch][e] = w;
-                        continue;
-                    }
-                    // T = fl32(acc*c - ref) rounded once (Alg. 1), or fl32(S - m) with
-                    // S = fl32(acc*c) (eq. (2), Exp2 HiF8)
-                    const float t0 = MODE == kModeE2E ? __builtin_fmaf(sacc[kt][ch * 8 + 2 * e], c, nref)
-                                                      : sacc[kt][ch * 8 + 2 * e] * c + nref;
-                    const float t1 = MODE == kModeE2E ? __builtin_fmaf(sacc[kt][ch * 8 + 2 * e + 1], c, nref)
-                                                      : sacc[kt][ch * 8 + 2 * e + 1] * c + nref;
-                    if constexpr (CT) {
-                        // two bf16 of P * 2^-kCodeBiasLog2
-                        w = ((uint32_t)ctab[hif8::f2u(t0) >> kTabShift] | ((uint32_t)ctab[hif8::f2u(t1) >> kTabShift] << 16)) << 4;
-                    } else {
-                        w = (uint32_t)tab[hif8::f2u(t0) >> kTabShift] | ((uint32_t)tab[hif8::f2u(t1) >> kTabShift] << 16);
-                    }
-                    pop[ch][e] = w;
-                    dl = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), ones, dl, false);
-                }
-            }
-            // X^T += V_j^T P^T over this tile's two 16-key chunks
-#pragma unroll
-            for (int ch = 0; ch < 2; ++ch) {
-                const int pc = 2 * kt + ch;
-#pragma unroll
-                for (int t = 0; t < kDT; ++t) {
-                    const char* pa = vt_lds + voff[t] + pc * 16 * C::kRowBytes;
-                    const s16x4 va = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LDS_PTR(s16x4, pa));
-                    const s16x4 vb = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LDS_PTR(s16x4, pa + 8 * C::kRowBytes));
-                    const u32x4 a = {__builtin_bit_cast(u32x2, va)[0], __builtin_bit_cast(u32x2, va)[1],
-                                     __builtin_bit_cast(u32x2, vb)[0], __builtin_bit_cast(u32x2, vb)[1]};
-                    oacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(pop[ch]), oacc[t], 0, 0, 0);
-                }
-            }
+            for (int i = tid; i < kTabEntries; i += C::kThreads) tab[i] = (uint16_t)(p.tab[i] >> 16);
         }
     }
+    load_q(fresh_args(), cur);
 
-    // epilogue: O = X / dX, lse = ln2 (ref + log2 dX) = ln2 (m + log2 d);
-    // with the compact table X and dX carry the factor 2^-kCodeBiasLog2
-    const float d = dl + __shfl_xor(dl, 32, 64);
-    const float dbias = (CT && MODE != kModeDefault) ? (float)kCodeBiasLog2 : 0.0f;
-    if (!row_ok) return;
-    float* orow = p.o + (((long long)b * p.Hq + h) * p.Sq + r) * D;
-    const bool empty = (ref == ninf);
-    const float inv = empty ? 0.0f : 1.0f / d;
+    const float ninf = -__builtin_huge_valf();
+    const float c = p.c;
+    const float lam = (float)p.lambda;
+    int sel = 0;                        // K/V buffer of the current key block
+
+    for (int rnd = 0;; ++rnd) {
+        const long long hoff_cur = kv_off(cur);
+
+        // this lane's query row: flat index f = r * G + h_local (computed
+        // afresh per item, from values the compiler cannot hoist out of the
+        // item loop)
+        int ln = lane, Gi = G;
+        opaque_v(ln);
+        opaque_s(Gi);
+        const int f = cur.tile * C::kTileRows + wave * kRowsPerWave + (ln & 31);
+        const bool row_ok = f < flat_rows;
+        const int r = row_ok ? f / Gi : 0;
+        const int h = cur.g * Gi + (row_ok ? f % Gi : 0);
+        const int kmax = row_ok ? (p.causal ? min(p.Sk - 1, r + off) : p.Sk - 1) : -1;
+        int kmax_wave_hi = kmax, kmax_wave_lo = row_ok ? kmax : 0x7fffffff;
 #pragma unroll
-    for (int t = 0; t < kDT; ++t)
-#pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-            f32x4 v;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) v[e] = oacc[t][q4 * 4 + e] * inv;
-            *reinterpret_cast<f32x4*>(orow + t * 32 + q4 * 8 + half * 4) = v;
+        for (int o = 1; o < 64; o <<= 1) {
+            kmax_wave_hi = max(kmax_wave_hi, __shfl_xor(kmax_wave_hi, o, 64));
+            kmax_wave_lo = min(kmax_wave_lo, __shfl_xor(kmax_wave_lo, o, 64));
         }
-    if (half == 0) {
-        if (p.lse) p.lse[((long long)b * p.Hq + h) * p.Sq + r] = empty ? ninf : 0.69314718055994531f * (ref + (log2f(d) + dbias));
-        if ((TILE ? trep : true) && n_visit) {
-            if (p.counters) {
-                atomicAdd(p.counters + 2 * ((long long)b * p.Hq + h) + 0, (unsigned long long)n_restart);
-                atomicAdd(p.counters + 2 * ((long long)b * p.Hq + h) + 1, (unsigned long long)n_visit);
+        // wave-uniform from here on: keeps the skip and mask branches scalar
+        kmax_wave_hi = __builtin_amdgcn_readfirstlane(kmax_wave_hi);
+        kmax_wave_lo = __builtin_amdgcn_readfirstlane(kmax_wave_lo);
+
+        // Alg. 1 state of this lane's row.  The output and the denominator are
+        // kept relative to the current block reference ref_j instead of the
+        // running maximum m_j: X_j = sum_{i<=j} 2^(ref_i - ref_j) P_i V_i and
+        // dX_j likewise, so O~_j = 2^(ref_j - m_j) X_j and d_j = 2^(ref_j - m_j) dX_j.
+        // The two power-of-two rescales of a block (2^(m_{j-1}-m_j) on the old
+        // state, 2^(ref_j - m_j) on the new block) fold into one exact rescale by
+        // 2^(ref_{j-1} - ref_j), needed only when the reference moves, and the
+        // normalisation O = O~/d = X/dX is unchanged.
+        float m = ninf;                 // running integer maximum m_j
+        float ref = ninf;               // current block reference
+        float dl = 0.0f;                // this lane's share of dX
+        unsigned n_restart = 0, n_visit = 0;
+        f32x16 oacc[kDT];
+#pragma unroll
+        for (int t = 0; t < kDT; ++t) oacc[t] = f32x16{};
+
+        for (int jb = 0; jb < cur.nblk; ++jb, sel ^= 1) {
+            const int key0 = jb * BLK;
+            const char* kt_lds = tiles + sel * 2 * C::kTileBytes;
+            const char* vt_lds = kt_lds + C::kTileBytes;
+            __builtin_amdgcn_s_waitcnt(0);                  // this wave's loads of block jb (and Q) landed
+            __syncthreads();                                // everyone's did; block jb-1 fully consumed
+            // the next block of this item, or the first block of the next
+            // item while the last one is computed
+            const bool last = jb + 1 == cur.nblk;
+            if (!last) {
+                issue_block(hoff_cur, jb + 1, sel ^ 1);
+            } else if constexpr (PERSIST) {
+                ItemGeo e;
+                if (item_of_round<BLK, C::kTileRows>(fresh_args(), rnd + 1, e) && e.nblk > 0)
+                    issue_block(kv_off(e), 0, sel ^ 1);
             }
-            if (p.tile_counts) {
-                const int R = p.restart_rows;
-                unsigned long long* tc =
-                    p.tile_counts + 2 * (((long long)b * p.Hq + h) * ((p.Sq + R - 1) / R) + r / R);
-                atomicAdd(tc + 0, (unsigned long long)n_restart);
-                atomicAdd(tc + 1, (unsigned long long)n_visit);
+            // A wave that sees nothing of the block skips it.  In a tile that
+            // spans waves it still takes part in the tile's exchange below, with
+            // no visible row (its row maximum stays -inf): the exchange has one
+            // barrier on one path, and the tile's representative lane counts the
+            // block whenever any row of the tile sees it.
+            const bool live = key0 <= kmax_wave_hi;
+            if (!live && !(TILE && xwave)) continue;
+
+            f32x16 sacc[kKT];
+#pragma unroll
+            for (int kt = 0; kt < kKT; ++kt) sacc[kt] = f32x16{};
+            float amax = ninf;
+            if (live) {
+            // S^T = K_j Q^T.  The wave raises its priority for the MFMA burst so
+            // that the two waves sharing a SIMD drift apart: one runs its QK^T
+            // MFMAs while the other runs the VALU softmax of its block.
+            __builtin_amdgcn_s_setprio(2);
+            if constexpr (F8) {
+                // FP8 E4M3 on both sides, unit block scales (E8M0 127): the
+                // dequantisation scales are folded into c
+#pragma unroll
+                for (int kk = 0; kk < kDK8; ++kk) {
+#pragma unroll
+                    for (int kt = 0; kt < kKT; ++kt) {
+                        const char* kp = kt_lds + kt * 32 * D;
+                        const u32x4 lo = *reinterpret_cast<const u32x4*>(kp + koff[2 * kk]);
+                        const u32x4 hi = *reinterpret_cast<const u32x4*>(kp + koff[2 * kk + 1]);
+                        sacc[kt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(cat8(lo, hi), qop8[kk], sacc[kt],
+                                                                                   0, 0, 0, 127, 0, 127);
+                    }
+                }
+            } else {
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int kk = 0; kk < kDK; ++kk) {
+                    const char* kp = kt_lds + koff[kk];
+#pragma unroll
+                    for (int kt = 0; kt < kKT; ++kt) {
+                        const u32x4 a = *reinterpret_cast<const u32x4*>(kp + kt * 32 * C::kRowBytes);
+                        sacc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(qop[kk]), sacc[kt],
+                                                                           0, 0, 0);
+                    }
+                }
+                // keep kKReads operand reads in flight ahead of the MFMAs that
+                // consume them (the default schedule keeps two, and the MFMAs
+                // wait on LDS latency)
+                constexpr int kKReads = 4;
+                __builtin_amdgcn_sched_group_barrier(0x100, kKReads, 0);          // LDS reads
+#pragma unroll
+                for (int i = 0; i < kDK * kKT - kKReads; ++i) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);            // one MFMA
+                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);            // one LDS read
+                }
+                __builtin_amdgcn_sched_group_barrier(0x008, kKReads, 0);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            __builtin_amdgcn_s_setprio(0);
+            // mask keys past kmax (causal diagonal, ragged tail); key of register
+            // i of tile kt: key0 + 32*kt + 8*(i/4) + 4*half + i%4
+            if (key0 + BLK - 1 > kmax_wave_lo) {
+                asm volatile("" ::: "memory");          // keep this a real branch (no if-conversion)
+                const int lim = kmax - key0 - 4 * half;
+#pragma unroll
+                for (int kt = 0; kt < kKT; ++kt)
+#pragma unroll
+                    for (int i = 0; i < 16; ++i)
+                        if (kt * 32 + 8 * (i / 4) + (i % 4) > lim) sacc[kt][i] = ninf;
+            }
+            // row maximum of the raw dot products (the scale c > 0 is monotone):
+            // a 3-way tree over this lane's 16*kKT scores, then lanes l and l^32
+            {
+                float mx[16 * kKT];
+#pragma unroll
+                for (int kt = 0; kt < kKT; ++kt)
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) mx[16 * kt + i] = sacc[kt][i];
+                amax = tree_max<16 * kKT>(mx);
+                amax = __builtin_fmaxf(amax, swap_halves(amax));
+            }
+            }  // live
+            float nref;
+            if constexpr (MODE == kModeE2E) {
+                // block-aware precision rescaling (Alg. 1), per row, branch-free.
+                // B0 blocks (and a first block with m = -inf) take the high-precision
+                // path; B1 blocks restart when ceil(rowmax T) > lambda, where rowmax of
+                // the 8-bit T = fl32(acc*c - m) is the 8-bit cast of the raw maximum's
+                // T (the cast is monotone).
+                const bool vis = (!TILE || row_ok) && amax != ninf;
+                const bool in_b0 = (jb < p.n_b0) || (p.b0_last && jb == kmax / BLK);
+                const bool forced = in_b0 || (m == ninf);
+                const float tq = hif8::round(__builtin_fmaf(amax, c, -m));
+                bool restart = forced || (ceilf(tq) > lam);
+                if constexpr (TILE) {
+                    // the tile restarts when any of its rows that see the block would
+                    const uint32_t wantb = (uint32_t)__ballot(vis && restart);
+                    const uint32_t visb = (uint32_t)__ballot(vis);
+                    const uint32_t b0b = (uint32_t)__ballot(vis && in_b0);
+                    uint32_t tw, tv, tb;
+                    if (!xwave) {
+                        tw = wantb & tmask;
+                        tv = visb & tmask;
+                        tb = b0b & tmask;
+                    } else {
+                        if (lane == 0) {
+                            tflag[wave][0] = wantb;
+                            tflag[wave][1] = visb;
+                            tflag[wave][2] = b0b;
+                        }
+                        __syncthreads();
+                        uint32_t a = 0, vv = 0, z = 0;
+                        for (int w = tw0; w < tw0 + twn; ++w) {
+                            a |= tflag[w][0];
+                            vv |= tflag[w][1];
+                            z |= tflag[w][2];
+                        }
+                        tw = a & tmask;
+                        tv = vv & tmask;
+                        tb = z & tmask;
+                    }
+                    restart = tw != 0u;
+                    if (trep && tv && !tb) {                    // a B1 tile-block
+                        ++n_visit;
+                        n_restart += restart ? 1u : 0u;
+                    }
+                } else {
+                    const bool b1 = vis && !in_b0;
+                    n_visit += b1 ? 1u : 0u;
+                    n_restart += (b1 && restart) ? 1u : 0u;
+                }
+                const float m_hi = __builtin_fmaxf(m, ceilf(amax * c));    // ceil(rowmax S), S in fp32
+                const float m_new = vis ? (restart ? m_hi : m + __builtin_fmaxf(0.0f, ceilf(tq))) : m;
+                const float ref_new = vis ? (restart ? m_hi : m) : ref;
+                const float f = (ref == ninf) ? 1.0f : exp2_int(ref - ref_new);
+                if (__any(f != 1.0f)) {
+        #pragma unroll
+                    for (int t = 0; t < kDT; ++t)
+        #pragma unroll
+                        for (int i = 0; i < 16; ++i) oacc[t][i] *= f;
+                }
+                dl *= f;
+                m = m_new;
+                ref = ref_new;
+    
+                // a row with no visible key so far keeps ref = -inf; its masked scores
+                // (acc = -inf) must still give T = -inf and P = 0
+                nref = (ref == ninf) ? 0.0f : -ref;
+            } else {
+                // eq. (2): real-valued running maximum m, rescale factor
+                // 2^(m_old - m) in fp32 (Default) or HiF8(2^HiF8(m_old - m)) (Exp2 HiF8)
+                const bool vis = amax != ninf;
+                const float m_new = vis ? __builtin_fmaxf(m, amax * c) : m;   // fl32(max acc * c) = max S
+                float f = 1.0f;
+                if (m != ninf) {
+                    const float x = m - m_new;
+                    if constexpr (MODE == kModeDefault) {
+                        f = __builtin_amdgcn_exp2f(x);
+                    } else {
+                        f = hif8::u2f((uint32_t)ctab[hif8::f2u(x) >> kTabShift] << 20) * 0x1p104f;
+                    }
+                }
+                if (__any(f != 1.0f)) {
+#pragma unroll
+                    for (int t = 0; t < kDT; ++t)
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) oacc[t][i] *= f;
+                }
+                dl *= f;
+                m = m_new;
+                ref = m_new;
+                nref = (m == ninf) ? 0.0f : -m;
+            }
+    
+            if (!live) continue;
+            const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+            for (int kt = 0; kt < kKT; ++kt) {
+                // P = HiF8(2^HiF8(T)), T = fl32(acc*c - ref), for this 32-key tile,
+                // packed as two bf16 B operands
+                u32x4 pop[2];
+#pragma unroll
+                for (int ch = 0; ch < 2; ++ch) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        uint32_t w;
+                        if constexpr (MODE == kModeDefault) {
+                            // P = 2^fl32(S - m) in fp32; bf16 into P V, fp32 into the sum
+                            const float p0 = __builtin_amdgcn_exp2f(sacc[kt][ch * 8 + 2 * e] * c + nref);
+                            const float p1 = __builtin_amdgcn_exp2f(sacc[kt][ch * 8 + 2 * e + 1] * c + nref);
+                            const bf16x2 pb = {(__bf16)p0, (__bf16)p1};
+                            w = __builtin_bit_cast(uint32_t, pb);
+                            dl += p0 + p1;
+                            pop[ch][e] = w;
+                            continue;
+                        }
+                        // T = fl32(acc*c - ref) rounded once (Alg. 1), or fl32(S - m) with
+                        // S = fl32(acc*c) (eq. (2), Exp2 HiF8)
+                        const float t0 = MODE == kModeE2E ? __builtin_fmaf(sacc[kt][ch * 8 + 2 * e], c, nref)
+                                                          : sacc[kt][ch * 8 + 2 * e] * c + nref;
+                        const float t1 = MODE == kModeE2E ? __builtin_fmaf(sacc[kt][ch * 8 + 2 * e + 1], c, nref)
+                                                          : sacc[kt][ch * 8 + 2 * e + 1] * c + nref;
+                        if constexpr (CT) {
+                            // two bf16 of P * 2^-kCodeBiasLog2
+                            w = ((uint32_t)ctab[hif8::f2u(t0) >> kTabShift] | ((uint32_t)ctab[hif8::f2u(t1) >> kTabShift] << 16)) << 4;
+                        } else {
+                            w = (uint32_t)tab[hif8::f2u(t0) >> kTabShift] | ((uint32_t)tab[hif8::f2u(t1) >> kTabShift] << 16);
+                        }
+                        pop[ch][e] = w;
+                        dl = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), ones, dl, false);
+                    }
+                }
+                // X^T += V_j^T P^T over this tile's two 16-key chunks
+#pragma unroll
+                for (int ch = 0; ch < 2; ++ch) {
+                    const int pc = 2 * kt + ch;
+#pragma unroll
+                    for (int t = 0; t < kDT; ++t) {
+                        const char* pa = vt_lds + voff[t] + pc * 16 * C::kRowBytes;
+                        const s16x4 va = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LDS_PTR(s16x4, pa));
+                        const s16x4 vb = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LDS_PTR(s16x4, pa + 8 * C::kRowBytes));
+                        const u32x4 a = {__builtin_bit_cast(u32x2, va)[0], __builtin_bit_cast(u32x2, va)[1],
+                                         __builtin_bit_cast(u32x2, vb)[0], __builtin_bit_cast(u32x2, vb)[1]};
+                        oacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(pop[ch]), oacc[t], 0, 0, 0);
+                    }
+                }
             }
         }
+
+        // epilogue: O = X / dX, lse = ln2 (ref + log2 dX) = ln2 (m + log2 d);
+        // with the compact table X and dX carry the factor 2^-kCodeBiasLog2
+        const float d = dl + __shfl_xor(dl, 32, 64);
+        const float dbias = (CT && MODE != kModeDefault) ? (float)kCodeBiasLog2 : 0.0f;
+        const kargs_ptr a = fresh_args();
+        if (row_ok) {
+            float* orow = a->o + (((long long)cur.b * a->Hq + h) * a->Sq + r) * D;
+            const bool empty = (ref == ninf);
+            const float inv = empty ? 0.0f : 1.0f / d;
+#pragma unroll
+            for (int t = 0; t < kDT; ++t)
+#pragma unroll
+                for (int q4 = 0; q4 < 4; ++q4) {
+                    f32x4 v;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) v[e] = oacc[t][q4 * 4 + e] * inv;
+                    *reinterpret_cast<f32x4*>(orow + t * 32 + q4 * 8 + half * 4) = v;
+                }
+            if (half == 0) {
+                if (a->lse)
+                    a->lse[((long long)cur.b * a->Hq + h) * a->Sq + r] =
+                        empty ? ninf : 0.69314718055994531f * (ref + (log2f(d) + dbias));
+                if ((TILE ? trep : true) && n_visit) {
+                    if (a->counters) {
+                        atomicAdd(a->counters + 2 * ((long long)cur.b * a->Hq + h) + 0, (unsigned long long)n_restart);
+                        atomicAdd(a->counters + 2 * ((long long)cur.b * a->Hq + h) + 1, (unsigned long long)n_visit);
+                    }
+                    if (a->tile_counts) {
+                        const int R = a->restart_rows;
+                        unsigned long long* tc =
+                            a->tile_counts + 2 * (((long long)cur.b * a->Hq + h) * ((a->Sq + R - 1) / R) + r / R);
+                        atomicAdd(tc + 0, (unsigned long long)n_restart);
+                        atomicAdd(tc + 1, (unsigned long long)n_visit);
+                    }
+                }
+            }
+        }
+        // the next item: its first key block is on its way (loaded during
+        // this item's last block); its Q is loaded now, behind the O stores
+        // (the first block waits for both)
+        ItemGeo nxt;
+        if (!PERSIST || !item_of_round<BLK, C::kTileRows>(a, rnd + 1, nxt)) break;
+        if (cur.nblk == 0 && nxt.nblk > 0) issue_block(kv_off(nxt), 0, sel);
+        load_q(a, nxt);
+        cur = nxt;
     }
 }
 
@@ -676,18 +791,35 @@ template <int D, int BLK, int NW, bool CT, int MODE, bool TILE = false, bool F8 
 hipError_t launch_one(const AttnParams& p, hipStream_t st)
 {
     using C = Cfg<D, BLK, NW>;
-    static bool attr_set = false;
-    if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute(
-            reinterpret_cast<const void*>(&baps_attn_fwd_kernel<D, BLK, NW, CT, MODE, TILE, F8>),
-            hipFuncAttributeMaxDynamicSharedMemorySize, C::kLdsBytes);
+    // D = 128 takes the persistent grid (one workgroup per CU, whose LDS it
+    // fills); D = 64 keeps one item per workgroup, which leaves the registers
+    // for two resident workgroups per CU
+    constexpr bool kPersist = D == 128;
+    const int lds = 4 * C::kTileBytes;
+    const void* fn = reinterpret_cast<const void*>(&baps_attn_fwd_kernel<D, BLK, NW, CT, MODE, TILE, F8, kPersist>);
+    // resident workgroups per CU, found once (the kernel's resources do not
+    // depend on the call)
+    static int per_cu = 0;
+    if (per_cu == 0) {
+        hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
         if (e != hipSuccess) return e;
-        attr_set = true;
+        int n = 0;
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, C::kThreads, lds);
+        if (e != hipSuccess) return e;
+        per_cu = n > 0 ? n : 1;
     }
+    int dev = 0, ncu = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    // persistent grid: every work item (query tile, key/value head, batch)
+    // on at most as many workgroups as the GPU holds at once
     const long long flat = (long long)p.Sq * (p.Hq / p.Hkv);
-    const dim3 grid((unsigned)((flat + C::kTileRows - 1) / C::kTileRows), (unsigned)p.Hkv, (unsigned)p.B);
-    hipLaunchKernelGGL((baps_attn_fwd_kernel<D, BLK, NW, CT, MODE, TILE, F8>), grid, dim3(C::kThreads), C::kLdsBytes,
-                       st, p);
+    const long long items = (flat + C::kTileRows - 1) / C::kTileRows * p.Hkv * p.B;
+    const long long slots = (long long)ncu * per_cu;
+    const unsigned grid = (unsigned)(kPersist && items > slots ? slots : items);
+    hipLaunchKernelGGL((baps_attn_fwd_kernel<D, BLK, NW, CT, MODE, TILE, F8, kPersist>), dim3(grid), dim3(C::kThreads),
+                       lds, st, p);
     return hipGetLastError();
 }
 

@@ -56,6 +56,7 @@ struct AttnParams {
     float* lse;                 // [B, Hq, Sq] or null
     const uint32_t* tab;        // score table (device)
     const uint8_t* ctab;        // compact code table (device), kCodeTableBytes bytes (entries, then zeros)
+    const uint8_t* ctabx;       // the compact code table expanded to all kTabEntries indices (device)
     unsigned long long* counters;  // [B*Hq][2] restarted / visited B1 tile-blocks, or null
     unsigned long long* tile_counts;  // [B*Hq][ceil(Sq/R)][2] the same per tile, or null
     int B, Hq, Hkv, Sq, Sk;
