@@ -20,6 +20,7 @@ SHAPES = [
     (3, 6, 3, 5000, 5000, 128, True, 128),     # 9 heads, 40 tiles each (last one 16 rows): 360 items
     (2, 8, 4, 4500, 2100, 128, False, 64),     # 8 heads, 36 tiles each (last one 40 rows): 288 items
     (1, 40, 8, 3000, 3000, 128, True, 32),     # 8 heads, G = 5 (a tile splits query positions): 472 items
+    (1, 32, 8, 4096, 4096, 128, True, 128),    # the Llama-3-8B prefill: 512 items, two per workgroup
 ]
 
 
@@ -32,11 +33,19 @@ def test_persistent_schedule(shape):
     q, k, v = make_qkv(B, Hq, Hkv, Sq, Sk, D, seed=sum(shape), outliers=True)
     o = torch.full((B, Hq, Sq, D), float("nan"), dtype=torch.float32, device="cuda:0")
     lse = torch.full((B, Hq, Sq), float("nan"), dtype=torch.float32, device="cuda:0")
+    cnt = torch.zeros((B * Hq, 2), dtype=torch.int64, device="cuda:0")
     print(f"persistent schedule {shape}: {-(-Sq * G // 256) * B * Hkv} items", flush=True)
-    baps.baps_attention_fwd(dev_bf16(q), dev_bf16(k), dev_bf16(v), o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block)
+    baps.baps_attention_fwd_ex(dev_bf16(q), dev_bf16(k), dev_bf16(v), o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block,
+                               restart_counts=cnt)
     torch.cuda.synchronize()
     assert not torch.isnan(o).any(), "rows never written"
     assert not torch.isnan(lse).any(), "lse never written"
+    # every (row, key block after the first) that a row sees is visited once:
+    # an item run twice (or skipped) moves its heads' totals
+    r = np.arange(Sq)
+    kmax = np.minimum(Sk - 1, r + Sk - Sq) if causal else np.full(Sq, Sk - 1)
+    want = int((np.clip(kmax, 0, None) // block).sum())
+    assert np.all(cnt[:, 1].cpu().numpy() == want), (cnt[:, 1].cpu().numpy(), want)
     o = o.cpu().numpy().reshape(-1, D).astype(np.float64)
     lse = lse.cpu().numpy().reshape(-1).astype(np.float64)
     # per (batch, head): a few positions, plus the positions of the last
