@@ -793,8 +793,9 @@ hipError_t launch_one(const AttnParams& p, hipStream_t st)
     using C = Cfg<D, BLK, NW>;
     // D = 128 takes the persistent grid (one workgroup per CU, whose LDS it
     // fills); D = 64 keeps one item per workgroup, which leaves the registers
-    // for two resident workgroups per CU
-    constexpr bool kPersist = D == 128;
+    // for two resident workgroups per CU, and so does tile-level restart,
+    // whose extra state would spill across the item loop
+    constexpr bool kPersist = D == 128 && !TILE;
     const int lds = 4 * C::kTileBytes;
     const void* fn = reinterpret_cast<const void*>(&baps_attn_fwd_kernel<D, BLK, NW, CT, MODE, TILE, F8, kPersist>);
     // resident workgroups per CU, found once (the kernel's resources do not
