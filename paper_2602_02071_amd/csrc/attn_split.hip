@@ -432,7 +432,25 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void split_pv_kernel(SplitParams s
     const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
     __syncthreads();                              // code table, references and counts published
 
-    for (int n = 0; n < nslots; ++n) {
+    // The raw dot products of kAccRun blocks are loaded together at the start
+    // of each run of blocks: the first use of a load waits for every older
+    // memory operation of the wave, which includes the V ring's loads in
+    // flight, so one load per block would let only one slot of the ring fly.
+    constexpr int kAccRun = 4;
+    for (int n0 = 0; n0 < nslots; n0 += kAccRun) {
+    f32x4 accr[kAccRun][2];
+#pragma unroll
+    for (int u = 0; u < kAccRun; ++u) {
+        const int key0 = (j0 + n0 + u) * BLK + wave * kSlotKeys;
+#pragma unroll
+        for (int t2 = 0; t2 < 2; ++t2)
+            accr[u][t2] = (ri.ok && n0 + u < nslots) ? *reinterpret_cast<const f32x4*>(acc_row + key0 + 16 * t2 + 4 * grp)
+                                                     : f32x4{ninf, ninf, ninf, ninf};
+    }
+#pragma unroll
+    for (int u = 0; u < kAccRun; ++u) {
+        const int n = n0 + u;
+        if (n >= nslots) break;
         const int jb = j0 + n;
         const int key0 = jb * BLK + wave * kSlotKeys;
         // this block's reference; the partials follow it with exact rescales
@@ -447,11 +465,7 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void split_pv_kernel(SplitParams s
         dl *= fac;
         if (rj != ninf) cur = rj;
         const float nref = (cur == ninf) ? 0.0f : -cur;
-        f32x4 sacc[2];
-#pragma unroll
-        for (int t2 = 0; t2 < 2; ++t2)
-            sacc[t2] = ri.ok ? *reinterpret_cast<const f32x4*>(acc_row + key0 + 16 * t2 + 4 * grp)
-                             : f32x4{ninf, ninf, ninf, ninf};
+        const f32x4* sacc = accr[u];
         u32x4 pop;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -476,6 +490,7 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void split_pv_kernel(SplitParams s
             oacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a), as_bf16x8(pop), oacc[t], 0, 0, 0);
         }
         if (issued < nslots) { issue_slot(issued); ++issued; }
+    }
     }
 
     // -- one sum over the waves (they share the references), then this
