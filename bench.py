@@ -70,23 +70,26 @@ def _spin_up(fn, min_ms):
 
 
 def _time_launches(fn, steps, warmup, spinup_ms=0.0):
+    """Spin-up, warm-up, then exactly `steps` calls of fn between two
+    synchronisations.  Returns (wall seconds of the timed calls, [mean GPU
+    time per call in ms]): one event pair on the launch stream brackets the
+    timed calls, so nothing is recorded between them (events between
+    launches leave gaps of their own on the stream)."""
     import torch
     _spin_up(fn, spinup_ms)
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
     st = torch.cuda.current_stream()
-    starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
-    ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
-    for i in range(steps):
-        starts[i].record(st)
+    e0.record(st)
+    for _ in range(steps):
         fn()
-        ends[i].record(st)
+    e1.record(st)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    per = [s.elapsed_time(e) for s, e in zip(starts, ends)]
-    return wall, per
+    return wall, [e0.elapsed_time(e1) / steps]
 
 
 def run_attention(cfg, steps, warmup, spinup_ms=0.0):
