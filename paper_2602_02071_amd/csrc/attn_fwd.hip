@@ -1,17 +1,21 @@
 // Fused BAPS attention forward (Alg. 1, the "E2E HiF8" workflow) for gfx950.
 //
-// Work split: a workgroup of NW waves owns 32*NW query rows of one key/value
-// head.  The rows are the flattened (query position, query head of the
-// group) pairs, so the Hq/Hkv query heads that share K/V share the
-// workgroup, and single-position decode packs its heads into one tile.  Each
-// wave owns 32 rows.
+// Work split: a work item is 32*NW query rows of one key/value head.  The
+// rows are the flattened (query position, query head of the group) pairs, so
+// the Hq/Hkv query heads that share K/V share the item, and single-position
+// decode packs its heads into one tile.  Each wave owns 32 rows.  At D = 128
+// the grid is persistent: one workgroup per CU takes a sequence of items
+// (item_at), and the first K/V block of the next item loads during the last
+// block of the current one; at D = 64 a workgroup takes one item and two of
+// them share a CU.
 //
 // Per key block j (the paper's key tile, visited in ascending order):
 //   - K_j and V_j arrive in LDS through asynchronous global->LDS loads into a
 //     double buffer: the loads of block j+1 are in flight while block j is
 //     computed.  Both tiles keep their natural [key][d] layout with the
-//     16-byte chunks of each row XOR-swizzled, so that the MFMA operand reads
-//     below are free of bank conflicts;
+//     16-byte chunks of each row XOR-swizzled, so that the ds_read_b128 K
+//     operand reads are free of bank conflicts (and the transposing V reads
+//     nearly so);
 //   - S^T = K_j Q^T on v_mfma_f32_32x32x16_bf16 with fp32 accumulation (Q
 //     stays in registers).  In the S^T layout a lane holds 16 keys of one
 //     query per 32-key tile, so a row maximum is an in-lane max plus one
