@@ -469,12 +469,15 @@ hipError_t launch_dec(const AttnParams& p, hipStream_t st)
 {
     using C = DCfg<D, BLK>;
     static_assert(C::kLdsBytes >= (C::kWaves - 1) * kRows * (D + 1) * 4, "merge buffer fits the ring");
-    static bool attr_set = false;
-    if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&baps_attn_decode_kernel<D, BLK, CT, MODE, F8>),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, C::kLdsBytes);
+    static DeviceOnce attr_set;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (!attr_set.is_done(dev)) {
+        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&baps_attn_decode_kernel<D, BLK, CT, MODE, F8>),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, C::kLdsBytes);
         if (e != hipSuccess) return e;
-        attr_set = true;
+        attr_set.mark(dev);
     }
     const long long flat = (long long)p.Sq * (p.Hq / p.Hkv);
     const dim3 grid((unsigned)((flat + kRows - 1) / kRows), (unsigned)p.Hkv, (unsigned)p.B);

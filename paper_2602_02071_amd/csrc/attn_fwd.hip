@@ -802,21 +802,23 @@ hipError_t launch_one(const AttnParams& p, hipStream_t st)
     constexpr bool kPersist = D == 128 && !TILE;
     const int lds = 4 * C::kTileBytes;
     const void* fn = reinterpret_cast<const void*>(&baps_attn_fwd_kernel<D, BLK, NW, CT, MODE, TILE, F8, kPersist>);
-    // resident workgroups per CU, found once (the kernel's resources do not
-    // depend on the call)
-    static int per_cu = 0;
+    int dev = 0, ncu = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    // resident workgroups per CU, found once per device ordinal below 64
+    // (the kernel's resources do not depend on the call; 0: not yet found)
+    static std::atomic<int> per_cu_of[64] = {};
+    int per_cu = (dev >= 0 && dev < 64) ? per_cu_of[dev].load(std::memory_order_relaxed) : 0;
     if (per_cu == 0) {
-        hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+        e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
         if (e != hipSuccess) return e;
         int n = 0;
         e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, C::kThreads, lds);
         if (e != hipSuccess) return e;
         per_cu = n > 0 ? n : 1;
+        if (dev >= 0 && dev < 64) per_cu_of[dev].store(per_cu, std::memory_order_relaxed);
     }
-    int dev = 0, ncu = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e == hipSuccess) e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
-    if (e != hipSuccess) return e;
     // persistent grid: every work item (query tile, key/value head, batch)
     // on at most as many workgroups as the GPU holds at once
     const long long flat = (long long)p.Sq * (p.Hq / p.Hkv);

@@ -642,9 +642,12 @@ hipError_t launch_split_db(const SplitParams& sp, hipStream_t st)
     using C = SCfg<D, BLK>;
     using PC = PCfg<D, BLK>;
     static_assert(C::kLdsBytes >= (C::kWaves - 1) * kRows * (D + 1) * 4, "merge buffer fits the ring");
-    static bool attr_set = false;
-    if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&split_scores_kernel<D, BLK, false>),
+    static DeviceOnce attr_set;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (!attr_set.is_done(dev)) {
+        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&split_scores_kernel<D, BLK, false>),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, C::kLdsBytes);
         if (e == hipSuccess)
             e = hipFuncSetAttribute(reinterpret_cast<const void*>(&split_scores_kernel<D, BLK, true>),
@@ -653,7 +656,7 @@ hipError_t launch_split_db(const SplitParams& sp, hipStream_t st)
             e = hipFuncSetAttribute(reinterpret_cast<const void*>(&split_pv_kernel<D, BLK>),
                                     hipFuncAttributeMaxDynamicSharedMemorySize, PC::kLdsBytes);
         if (e != hipSuccess) return e;
-        attr_set = true;
+        attr_set.mark(dev);
     }
     const AttnParams& p = sp.a;
     if (sp.bps < 1 || sp.bps > kSplitMaxBps || sp.bstride % kWinBlocks || sp.bstride < sp.nblk ||
@@ -666,7 +669,7 @@ hipError_t launch_split_db(const SplitParams& sp, hipStream_t st)
         hipLaunchKernelGGL((split_scores_kernel<D, BLK, true>), grid, dim3(64 * C::kWaves), C::kLdsBytes, st, sp);
     else
         hipLaunchKernelGGL((split_scores_kernel<D, BLK, false>), grid, dim3(64 * C::kWaves), C::kLdsBytes, st, sp);
-    hipError_t e = hipGetLastError();
+    e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((split_pv_kernel<D, BLK>), grid, dim3(PC::kThreads), PC::kLdsBytes, st, sp);
     e = hipGetLastError();

@@ -3,9 +3,27 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "hif8.hpp"
 
 namespace baps {
+
+// Host-side set-up done once per device and kernel (a launch attribute, an
+// occupancy query): one bit per device ordinal below 64, set once the step
+// succeeded there.  Concurrent first calls may both run the step, which is
+// idempotent.  Ordinals from 64 up run it on every call.
+struct DeviceOnce {
+    std::atomic<unsigned long long> done{0};
+    bool is_done(int dev) const
+    {
+        return dev >= 0 && dev < 64 && (done.load(std::memory_order_acquire) >> dev & 1ull);
+    }
+    void mark(int dev)
+    {
+        if (dev >= 0 && dev < 64) done.fetch_or(1ull << dev, std::memory_order_release);
+    }
+};
 
 typedef __bf16 bf16x8 __attribute__((__vector_size__(8 * sizeof(__bf16))));
 typedef float f32x16 __attribute__((__vector_size__(16 * sizeof(float))));

@@ -295,15 +295,15 @@ hipError_t launch_softmax_block(const SoftmaxBlockParams& p, hipStream_t st)
                      ((uintptr_t)p.codes % 4 == 0) && p.block <= 256;
     if (vec) {
         // one 1024-thread workgroup per CU when the rows fill every CU
-        static int ncu_of[64] = {};                 // CU count per device, read once
+        static std::atomic<int> ncu_of[64] = {};    // CU count per device, read once
         int dev = 0;
         hipError_t e = hipGetDevice(&dev);
         if (e != hipSuccess) return e;
-        int ncu = (dev >= 0 && dev < 64) ? ncu_of[dev] : 0;
+        int ncu = (dev >= 0 && dev < 64) ? ncu_of[dev].load(std::memory_order_relaxed) : 0;
         if (ncu == 0) {
             e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
             if (e != hipSuccess) return e;
-            if (dev >= 0 && dev < 64) ncu_of[dev] = ncu;
+            if (dev >= 0 && dev < 64) ncu_of[dev].store(ncu, std::memory_order_relaxed);
         }
         const long long wg1024 = (p.rows + 4 * 16 - 1) / (4 * 16);
         return wg1024 >= ncu ? launch_block4<1024>(p, st) : launch_block4<256>(p, st);
