@@ -65,9 +65,9 @@ def _load():
     L.orc_hif8_round.restype = d
     L.orc_hif8_round.argtypes = [d, i32]
     L.orc_e4m3_encode.restype = i32
-    L.orc_e4m3_encode.argtypes = [d]
+    L.orc_e4m3_encode.argtypes = [d, i32]
     L.orc_e5m2_encode.restype = i32
-    L.orc_e5m2_encode.argtypes = [d]
+    L.orc_e5m2_encode.argtypes = [d, i32]
     L.orc_e4m3_decode.restype = d
     L.orc_e4m3_decode.argtypes = [i32]
     L.orc_e5m2_decode.restype = d
@@ -89,11 +89,11 @@ def _load():
                                 i32, i32, i32, i32, d, P, i64, P, P, P, i32]
     L.orc_attention_ex.restype = i32
     L.orc_attention_ex.argtypes = [P, P, P, i32, i32, i32, i32, i32, i32, i32, i32,
-                                   i32, i32, i32, i32, d, P, i64, P, P, P, P, d, ctypes.c_uint64, i32, i32, i32]
+                                   i32, i32, i32, i32, d, P, i64, P, P, P, P, i32, i32, i32, P, i64, P, i64]
     L.orc_attention_tiles.restype = i32
     L.orc_attention_tiles.argtypes = [P, P, P, i32, i32, i32, i32, i32, i32, i32, i32,
-                                      i32, i32, i32, i32, i32, i32, d, P, i64, P, P, P, P, P, d,
-                                      ctypes.c_uint64, i32, i32]
+                                      i32, i32, i32, i32, i32, i32, d, P, i64, P, P, P, P, P, i32, i32,
+                                      P, i64, P, i64]
     L.orc_exact_attention.restype = i32
     L.orc_exact_attention.argtypes = [P, P, P, i32, i32, i32, i32, i32, i32, i32,
                                       d, P, i64, P, P, i32]
@@ -120,32 +120,38 @@ def hif8_decode(codes) -> np.ndarray:
     return table[codes]
 
 
-def hif8_encode(x, saturate: bool = True, nthreads: int = 0) -> np.ndarray:
-    """Round-to-nearest (ties away) HiF8 code of each fp32 value."""
+def _hif8_flags(saturate, ties_even):
+    return (1 if saturate else 0) | (2 if ties_even else 0)
+
+
+def hif8_encode(x, saturate: bool = True, nthreads: int = 0, ties_even: bool = False) -> np.ndarray:
+    """Round-to-nearest HiF8 code of each fp32 value (ties away from zero, or
+    to even)."""
     L = _load()
     x = np.ascontiguousarray(np.asarray(x, dtype=np.float32))
     out = np.empty(x.shape, dtype=np.uint8)
-    L.orc_hif8_encode_f32(_ptr(x), _ptr(out), x.size, int(saturate), nthreads)
+    L.orc_hif8_encode_f32(_ptr(x), _ptr(out), x.size, _hif8_flags(saturate, ties_even), nthreads)
     return out
 
 
-def hif8_encode_scalar(x: float, saturate: bool = True) -> int:
-    return int(_load().orc_hif8_encode(float(x), int(saturate)))
+def hif8_encode_scalar(x: float, saturate: bool = True, ties_even: bool = False) -> int:
+    return int(_load().orc_hif8_encode(float(x), _hif8_flags(saturate, ties_even)))
 
 
-def hif8_round(x, saturate: bool = True) -> np.ndarray:
+def hif8_round(x, saturate: bool = True, ties_even: bool = False) -> np.ndarray:
     """The value each fp32 input takes after the 8-bit cast."""
-    return hif8_decode(hif8_encode(x, saturate))
+    return hif8_decode(hif8_encode(x, saturate, ties_even=ties_even))
 
 
-def check_patterns(start: int, codes: np.ndarray, saturate: bool = True, nthreads: int = 0):
+def check_patterns(start: int, codes: np.ndarray, saturate: bool = True, nthreads: int = 0,
+                   ties_even: bool = False):
     """Compare codes[i] with the oracle's code for fp32 bit pattern start+i.
     Returns (mismatch count, first mismatching index or -1)."""
     L = _load()
     codes = np.ascontiguousarray(codes, dtype=np.uint8)
     first = ctypes.c_int64(-1)
     bad = L.orc_hif8_check_patterns(ctypes.c_uint64(start), codes.size, _ptr(codes),
-                                    int(saturate), nthreads, ctypes.byref(first))
+                                    _hif8_flags(saturate, ties_even), nthreads, ctypes.byref(first))
     return int(bad), int(first.value)
 
 
@@ -174,12 +180,16 @@ def round_fp16(y: float) -> float:
     return float(_load().orc_round_fp16(float(y)))
 
 
-def e4m3_encode(x: float) -> int:
-    return int(_load().orc_e4m3_encode(float(x)))
+def e4m3_encode(x: float, saturate: bool = True) -> int:
+    """OCP FP8 E4M3 code of x: nearest value, ties to even; beyond the
+    largest finite value 448 the NaN code unless saturate."""
+    return int(_load().orc_e4m3_encode(float(x), int(bool(saturate))))
 
 
-def e5m2_encode(x: float) -> int:
-    return int(_load().orc_e5m2_encode(float(x)))
+def e5m2_encode(x: float, saturate: bool = True) -> int:
+    """OCP FP8 E5M2 code of x: nearest value, ties to even; overflow to
+    +-Inf unless saturate."""
+    return int(_load().orc_e5m2_encode(float(x), int(bool(saturate))))
 
 
 def e4m3_decode(c: int) -> float:
@@ -208,8 +218,8 @@ def _rows(rows, total):
 
 
 def attention(q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, block, mode=E2E_HIF8, lam=1, n_b0=1,
-              literal_else=False, scale_log2=0.0, rows=None, nthreads=0, margin=False, jitter=0.0,
-              jitter_seed=0, pv_bf16=False, restart_rows=1, b0_last=False, visits=False, qk_fp8=False):
+              literal_else=False, scale_log2=0.0, rows=None, nthreads=0, margin=False, pv_bf16=False,
+              restart_rows=1, b0_last=False, visits=False, tie_even=False, acc=None, refs=False):
     """Attention rows in one of the paper's setups.
 
     q: [B,Hq,Sq,D], k/v: [B,Hkv,Sk,D] bf16 bit patterns.  rows: global row
@@ -218,21 +228,28 @@ def attention(q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, block, mode=E2E_HIF8, lam=
     per-row decision margin when margin=True: how far the row's 8-bit
     decisions sit from a rounding boundary, in units of the fp32 dot-product
     accumulation error bound (>= 1: every valid high-precision S yields this
-    result).  jitter moves every dot product by jitter times that bound
-    (same direction for jitter_seed 0, random signs otherwise).  pv_bf16 (the
-    setups of eq. (2) only): P enters the P V product rounded to bf16, the
-    input precision of a matrix unit, while the denominator sums P as
-    computed.
+    result).  pv_bf16 (the setups of eq. (2) only): P enters the P V product
+    rounded to bf16, the input precision of a matrix unit, while the
+    denominator sums P as computed.  tie_even: the 8-bit casts of the
+    softmax round ties to even (else away from zero).
+
+    acc: float32 [n, >= Sk] -- the high-precision dot products q.k of each
+    requested row (row i, key c at acc[i, c]; only the keys the row sees are
+    read) in place of fl32 of the exact ones: the result of the setup on that
+    S, e.g. a matrix unit's own sums.  refs=True also returns the reference
+    of every requested row at every key block it sees ([n, ceil(Sk/block)],
+    NaN elsewhere): Alg. 1's m~ (the value T = S - m~ is taken against), or
+    the running maximum m after the block in the eq. (2) setups.
 
     restart_rows / b0_last / visits (Alg. 1 setups only) take the tile-level
     path: the restart decision is shared by restart_rows consecutive query
     positions of one head, B0 also holds each row's last key block when
     b0_last, and the counts are per tile: restarts[n] (and, with visits,
     one more array of visited B1 tile-blocks before the margin) hold the
-    row's tile's restarted B1 tile-blocks.
+    row's tile's restarted B1 tile-blocks.  With acc, every row of every
+    tile touched must be requested.
 
-    qk_fp8: q and k carry FP8 E4M3 values (as bf16 patterns, e4m3_to_bf16):
-    the margins and jitters use the FP8 matrix unit's accumulation bound."""
+    Extra outputs come in the order visits, margin, refs."""
     L = _load()
     q, k, v = _bits(q), _bits(k), _bits(v)
     rows = _rows(rows, B * Hq * Sq)
@@ -241,27 +258,53 @@ def attention(q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, block, mode=E2E_HIF8, lam=
     lse = np.zeros(n, dtype=np.float64)
     nrs = np.zeros(n, dtype=np.int32)
     mg = np.zeros(n, dtype=np.float64) if margin else None
+    nblk = (Sk + block - 1) // block if block > 0 else 0
+    ref = np.full((n, max(nblk, 1)), np.nan, dtype=np.float64) if refs else None
+    ld_ref = ref.shape[1] if refs else 0
+    if acc is not None:
+        acc = np.ascontiguousarray(acc, dtype=np.float32)
+        if acc.ndim != 2 or acc.shape[0] != n or acc.shape[1] < Sk:
+            raise ValueError("acc must be float32 [len(rows), >= Sk]")
+        ld_acc = acc.shape[1]
+    else:
+        ld_acc = 0
     if restart_rows != 1 or b0_last or visits:
         nvs = np.zeros(n, dtype=np.int32)
         st = L.orc_attention_tiles(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, Sq, Sk, D, int(causal), block,
                                    int(mode), int(lam), int(n_b0), int(bool(b0_last)), int(restart_rows),
                                    int(literal_else), float(scale_log2), _ptr(rows), n, _ptr(o), _ptr(lse),
-                                   _ptr(nrs), _ptr(nvs), _ptr(mg), float(jitter),
-                                   ctypes.c_uint64(int(jitter_seed)), int(nthreads), int(bool(qk_fp8)))
+                                   _ptr(nrs), _ptr(nvs), _ptr(mg), int(nthreads), int(bool(tie_even)),
+                                   _ptr(acc), ld_acc, _ptr(ref), ld_ref)
         if st:
             raise ValueError("oracle rejected the attention arguments")
-        out = (o, lse, nrs) + ((nvs,) if visits else ()) + ((mg,) if margin else ())
-        return out
+        return (o, lse, nrs) + ((nvs,) if visits else ()) + ((mg,) if margin else ()) + ((ref,) if refs else ())
     st = L.orc_attention_ex(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, Sq, Sk, D, int(causal), block,
                             int(mode), int(lam), int(n_b0), int(literal_else), float(scale_log2),
-                            _ptr(rows), n, _ptr(o), _ptr(lse), _ptr(nrs), _ptr(mg), float(jitter),
-                            ctypes.c_uint64(int(jitter_seed)), int(nthreads), int(bool(pv_bf16)),
-                            int(bool(qk_fp8)))
+                            _ptr(rows), n, _ptr(o), _ptr(lse), _ptr(nrs), _ptr(mg), int(nthreads),
+                            int(bool(pv_bf16)), int(bool(tie_even)), _ptr(acc), ld_acc, _ptr(ref), ld_ref)
     if st:
         raise ValueError("oracle rejected the attention arguments")
-    if margin:
-        return o, lse, nrs, mg
-    return o, lse, nrs
+    return (o, lse, nrs) + ((mg,) if margin else ()) + ((ref,) if refs else ())
+
+
+def acc_bound(q, k, B, Hq, Hkv, Sq, Sk, D, rows):
+    """The accumulation error bound of each requested row's dot products,
+    [n, Sk] fp64: gamma_(D-1) * sum_d |q_d k_d| with gamma_n = n u/(1 - n u),
+    u = 2^-24 -- how far a sum of the D exact products formed with fp32
+    round-to-nearest additions, in any order, can lie from the exact q.k."""
+    def f64(bits):
+        return (_bits(bits).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    rows = _rows(rows, B * Hq * Sq)
+    qf = f64(q).reshape(B * Hq * Sq, D)[rows]
+    kf = f64(k).reshape(B, Hkv, Sk, D)
+    b = rows // (Hq * Sq)
+    g = (rows // Sq) % Hq // (Hq // Hkv)
+    n_, u = max(D - 1, 0), 2.0 ** -24
+    gamma = n_ * u / (1 - n_ * u)
+    out = np.empty((rows.size, Sk), dtype=np.float64)
+    for i in range(rows.size):
+        out[i] = gamma * (np.abs(kf[b[i], g[i]]) @ np.abs(qf[i]))
+    return out
 
 
 def e4m3_to_bf16(codes) -> np.ndarray:

@@ -27,7 +27,8 @@
  *       exponent with implicit leading one | mantissa; Inf = 0x6F/0xEF,
  *       NaN = 0x80, zero = 0x00.
  *   R2  rounding to nearest, ties away from zero, straight from the input
- *       value (one rounding, no FP16 intermediate).
+ *       value (one rounding, no FP16 intermediate); ties to even on request.
+ *       The OCP FP8 formats of the Table 1 setups round ties to even.
  *   R3  finite overflow saturates to +-2^15; +-Inf stays +-Inf.
  *   R5  the 8-bit exp2 is E8(t) = HiF8(exp2(t)) with exp2 in fp64.
  *   R6  the integer row maximum uses ceil (Alg. 1).
@@ -44,7 +45,10 @@
  *   R15 S = fl32(acc * c) with acc = fl32(q.k) (dot product in fp64, rounded
  *       once) and c = fl32(log2(e)/sqrt(d)); in the fused pass the product
  *       and the subtraction of eq. (3) are one operation rounded once:
- *       T = fl32(acc * c - ref).
+ *       T = fl32(acc * c - ref).  Any acc within the fp32 summation bound of
+ *       the exact q.k is an equally valid high-precision S: the caller may
+ *       supply its own (a matrix unit's sums) and get the setup's result on
+ *       exactly that S.
  *   R17 query head h reads key/value head h / (Hq/Hkv).
  */
 #define _GNU_SOURCE
@@ -70,6 +74,9 @@ typedef struct {
     double over_next;      /* nominal value after the maximum: a value rounds
                               to +Inf (non-saturating) when it is at least the
                               midpoint between the maximum and this value    */
+    int    ties_even;      /* a value exactly halfway between two neighbours
+                              goes to the one with an even significand (else
+                              away from zero)                                */
 } orc_format;
 
 /* HiF8 decoding from the field layout (R1).  Returns the value of a code;
@@ -121,10 +128,10 @@ static double e5m2_decode(int code)
     return s ? -v : v;
 }
 
-static orc_format F_HIF8, F_E4M3, F_E5M2;
+static orc_format F_HIF8, F_HIF8_EVEN, F_E4M3, F_E5M2;
 
 static void build_format(orc_format* f, double (*dec)(int), int inf_code, int nan_code,
-                         double over_next)
+                         double over_next, int ties_even)
 {
     int n = 0;
     for (int c = 0; c < 128; ++c) {
@@ -136,26 +143,38 @@ static void build_format(orc_format* f, double (*dec)(int), int inf_code, int na
         f->val[i] = v; f->code[i] = c;
     }
     f->n = n; f->neg_bit = 0x80; f->inf_code = inf_code; f->nan_code = nan_code;
-    f->over_next = over_next;
+    f->over_next = over_next; f->ties_even = ties_even;
 }
 
 __attribute__((constructor)) static void init_formats(void)
 {
-    build_format(&F_HIF8, orc_hif8_decode, 0x6f, 0x80, 1.5 * 32768.0);
-    build_format(&F_E4M3, e4m3_decode, -1, 0x7f, 480.0);
-    build_format(&F_E5M2, e5m2_decode, 0x7c, 0x7f, 65536.0);
+    /* HiF8: ties away from zero (R2), or to even when asked; OCP E4M3 and
+     * E5M2: to nearest even, the rounding of the OCP 8-bit float definition */
+    build_format(&F_HIF8, orc_hif8_decode, 0x6f, 0x80, 1.5 * 32768.0, 0);
+    build_format(&F_HIF8_EVEN, orc_hif8_decode, 0x6f, 0x80, 1.5 * 32768.0, 1);
+    build_format(&F_E4M3, e4m3_decode, -1, 0x7f, 480.0, 1);
+    build_format(&F_E5M2, e5m2_decode, 0x7c, 0x7f, 65536.0, 1);
 }
 
-/* Round-to-nearest by search over the value set (R2: ties away from zero).
- * Returns the index of the chosen non-negative value in f->val, or -1 for
- * +Inf.  'a' is a non-negative magnitude (may be +Inf). */
+/* Round-to-nearest by search over the value set.  At an exact tie the
+ * format's rule decides: away from zero (HiF8, R2), or the neighbour whose
+ * significand is even, i.e. whose value is an even multiple of the spacing
+ * between the two neighbours (this is IEEE's ties-to-even; it sends a tie
+ * between the largest value of a binade and the next power of two up, and a
+ * tie between zero and the smallest value down to zero).  Returns the index
+ * of the chosen non-negative value in f->val, or -1 for an overflow (+Inf,
+ * or NaN in a format without Inf).  'a' is a non-negative magnitude (may be
+ * +Inf; without saturation +Inf overflows). */
 static int nearest_index(const orc_format* f, double a, int saturate)
 {
     int top = f->n - 1;
-    if (isinf(a)) return f->inf_code >= 0 ? -1 : top;
+    if (isinf(a)) return (f->inf_code >= 0 || !saturate) ? -1 : top;
     if (a >= f->val[top]) {
-        if (saturate || f->inf_code < 0) return top;
-        return a >= 0.5 * (f->val[top] + f->over_next) ? -1 : top;
+        if (saturate) return top;
+        const double mid = 0.5 * (f->val[top] + f->over_next);
+        if (a == mid && f->ties_even)
+            return fmod(f->val[top] / (f->over_next - f->val[top]), 2.0) == 0.0 ? top : -1;
+        return a >= mid ? -1 : top;
     }
     /* largest i with val[i] <= a */
     int lo = 0, hi = top;
@@ -164,6 +183,8 @@ static int nearest_index(const orc_format* f, double a, int saturate)
         if (f->val[mid] <= a) lo = mid; else hi = mid;
     }
     double midpoint = 0.5 * (f->val[lo] + f->val[lo + 1]);   /* exact in fp64 */
+    if (a == midpoint && f->ties_even)
+        return fmod(f->val[lo] / (f->val[lo + 1] - f->val[lo]), 2.0) == 0.0 ? lo : lo + 1;
     return a >= midpoint ? lo + 1 : lo;
 }
 
@@ -171,6 +192,7 @@ static int fmt_encode(const orc_format* f, double x, int saturate)
 {
     if (isnan(x)) return f->nan_code;
     int i = nearest_index(f, fabs(x), saturate);
+    if (i < 0 && f->inf_code < 0) return f->nan_code;         /* overflow of a format without Inf */
     int code = i < 0 ? f->inf_code : f->code[i];
     if (code == 0) return 0;                       /* -0 has no code of its own */
     return signbit(x) ? (code | f->neg_bit) : code;
@@ -181,14 +203,21 @@ static double fmt_round(const orc_format* f, double x, int saturate)
 {
     if (isnan(x)) return x;
     int i = nearest_index(f, fabs(x), saturate);
+    if (i < 0 && f->inf_code < 0) return NAN;
     double a = i < 0 ? INFINITY : f->val[i];
     return signbit(x) ? -a : a;
 }
 
-int orc_hif8_encode(double x, int saturate) { return fmt_encode(&F_HIF8, x, saturate); }
-double orc_hif8_round(double x, int saturate) { return fmt_round(&F_HIF8, x, saturate); }
-int orc_e4m3_encode(double x) { return fmt_encode(&F_E4M3, x, 1); }
-int orc_e5m2_encode(double x) { return fmt_encode(&F_E5M2, x, 1); }
+/* flags of the HiF8 cast: ORC_SAT clamps finite overflow to the largest
+ * value, ORC_EVEN rounds ties to even (else away from zero) */
+#define ORC_SAT 1
+#define ORC_EVEN 2
+static const orc_format* hif8_fmt(int flags) { return (flags & ORC_EVEN) ? &F_HIF8_EVEN : &F_HIF8; }
+
+int orc_hif8_encode(double x, int flags) { return fmt_encode(hif8_fmt(flags), x, flags & ORC_SAT); }
+double orc_hif8_round(double x, int flags) { return fmt_round(hif8_fmt(flags), x, flags & ORC_SAT); }
+int orc_e4m3_encode(double x, int saturate) { return fmt_encode(&F_E4M3, x, saturate); }
+int orc_e5m2_encode(double x, int saturate) { return fmt_encode(&F_E5M2, x, saturate); }
 double orc_e4m3_decode(int c) { return e4m3_decode(c); }
 double orc_e5m2_decode(int c) { return e5m2_decode(c); }
 
@@ -242,21 +271,21 @@ static void parallel_for(int64_t n, int nthreads, int64_t chunk, range_fn fn, vo
 /* Bulk encode and the exhaustive check helper                               */
 /* ------------------------------------------------------------------------ */
 
-typedef struct { const float* x; uint8_t* out; int sat; } enc_ctx;
+typedef struct { const float* x; uint8_t* out; int flags; } enc_ctx;
 
 static void enc_range(void* p, int64_t i0, int64_t i1)
 {
     enc_ctx* c = (enc_ctx*)p;
-    for (int64_t i = i0; i < i1; ++i) c->out[i] = (uint8_t)fmt_encode(&F_HIF8, (double)c->x[i], c->sat);
+    for (int64_t i = i0; i < i1; ++i) c->out[i] = (uint8_t)orc_hif8_encode((double)c->x[i], c->flags);
 }
 
-void orc_hif8_encode_f32(const float* x, uint8_t* out, int64_t n, int saturate, int nthreads)
+void orc_hif8_encode_f32(const float* x, uint8_t* out, int64_t n, int flags, int nthreads)
 {
-    enc_ctx c = { x, out, saturate };
+    enc_ctx c = { x, out, flags };
     parallel_for(n, nthreads, 1 << 16, enc_range, &c);
 }
 
-typedef struct { uint64_t start; const uint8_t* got; int sat; int64_t bad; int64_t first_bad; } chk_ctx;
+typedef struct { uint64_t start; const uint8_t* got; int flags; int64_t bad; int64_t first_bad; } chk_ctx;
 
 static void chk_range(void* p, int64_t i0, int64_t i1)
 {
@@ -265,7 +294,7 @@ static void chk_range(void* p, int64_t i0, int64_t i1)
     for (int64_t i = i0; i < i1; ++i) {
         uint32_t bits = (uint32_t)(c->start + (uint64_t)i);
         float x; memcpy(&x, &bits, 4);
-        int want = fmt_encode(&F_HIF8, (double)x, c->sat);
+        int want = orc_hif8_encode((double)x, c->flags);
         if (want != c->got[i]) { if (first < 0) first = i; ++bad; }
     }
     if (bad) {
@@ -279,10 +308,10 @@ static void chk_range(void* p, int64_t i0, int64_t i1)
 /* Compares codes[i] against the encoding of the fp32 bit pattern start + i,
  * for i < count.  Returns the number of mismatches; *first_bad gets the
  * first mismatching index (or -1). */
-int64_t orc_hif8_check_patterns(uint64_t start, int64_t count, const uint8_t* codes, int saturate,
+int64_t orc_hif8_check_patterns(uint64_t start, int64_t count, const uint8_t* codes, int flags,
                                 int nthreads, int64_t* first_bad)
 {
-    chk_ctx c = { start, codes, saturate, 0, -1 };
+    chk_ctx c = { start, codes, flags, 0, -1 };
     parallel_for(count, nthreads, 1 << 18, chk_range, &c);
     if (first_bad) *first_bad = c.first_bad;
     return c.bad;
@@ -393,10 +422,18 @@ typedef struct {
     double *o, *lse;
     int32_t* nrestart;      /* restarted B1 blocks per row (nullable) */
     double* margin;         /* decision margin per row (nullable), see row_alg1 */
-    double jitter;          /* move each dot product by jitter * its error bound */
-    uint64_t jitter_seed;   /* 0: every dot product moves the same way; else random signs */
     int pv_bf16;            /* eq. (2) setups: P enters the P V product rounded to bf16 */
-    int qk_fp8;             /* q and k carry FP8 E4M3 values: the FP8 matrix unit's error bound */
+    int hif8_flags;         /* the 8-bit cast of T (Alg. 1) and of x (Exp2 HiF8): ORC_SAT,
+                               plus ORC_EVEN for ties to even */
+    const float* acc_in;    /* nullable: the high-precision q.k of requested row i and key c
+                               is acc_in[i * ld_acc + c] instead of fl32(q.k) */
+    int64_t ld_acc;
+    double* ref_out;        /* nullable: the reference of requested row i at its visible key
+                               block j goes to ref_out[i * ld_ref + j] (Alg. 1: the m~ that
+                               T = S - m~ is taken against; eq. (2): the running maximum m
+                               after block j) */
+    int64_t ld_ref;
+    int err;                /* set when acc_in lacks a row that a tile decision needs */
 } attn_job;
 
 static inline double bf16_to_double(uint16_t b)
@@ -421,12 +458,6 @@ static double dot64(const uint16_t* a, const uint16_t* b, int D)
     return s;
 }
 
-/* A matrix unit accumulating q.k in fp32 lands within ACC_ERR * 2^-24 *
- * sum_d |q_d k_d| of the exact dot product (the measured worst case on
- * gfx950 bf16 MFMA is about 6 of these units).  Every high-precision S
- * within that bound is an equally valid "S in high precision" of Alg. 1. */
-#define ACC_ERR 16.0
-
 static double abs_dot64(const uint16_t* a, const uint16_t* b, int D)
 {
     double s = 0.0;
@@ -434,37 +465,37 @@ static double abs_dot64(const uint16_t* a, const uint16_t* b, int D)
     return s;
 }
 
-/* The error bound of the matrix unit's dot product, in the units of acc.
- * bf16 operands: fp32 accumulation, ACC_ERR * 2^-24 * sum |q_d k_d|.  FP8
- * operands (the gfx950 FP8 matrix instructions): each step of 64 values of d
- * is summed with about 12 bits below its largest product (measured up to
- * 5700 units of 2^-24 * (largest |q_d k_d| of each step + |q.k|) over
- * normal and outlier-channel data, for both the 32x32x64 and the 16x16x128
- * forms); the bound is 2^-10 times that, plus the fp32 term. */
-static double acc_err(const attn_job* J, const uint16_t* a, const uint16_t* b, int D)
+/* Error bound of a matrix unit's dot product acc = q.k: the D products are
+ * exact in fp32 (a bf16 x bf16 product has at most 16 significant bits), and
+ * a sum of D terms formed with fp32 round-to-nearest additions, in any order,
+ * lies within gamma_(D-1) * sum_d |q_d k_d| of the exact sum, where
+ * gamma_n = n u / (1 - n u) and u = 2^-24 (the standard bound of recursive
+ * summation; Higham, Accuracy and Stability of Numerical Algorithms, 2nd
+ * ed., Sec. 4.2).  Every S within that bound is an equally valid "S in high
+ * precision" of Alg. 1. */
+static double acc_err(const uint16_t* a, const uint16_t* b, int D)
 {
-    double e = ACC_ERR * ldexp(abs_dot64(a, b, D), -24);
-    if (J->qk_fp8) {
-        double gm = 0.0;
-        for (int g0 = 0; g0 < D; g0 += 64) {
-            double mx = 0.0;
-            for (int i = g0; i < g0 + 64 && i < D; ++i) {
-                const double p = fabs(bf16_to_double(a[i]) * bf16_to_double(b[i]));
-                if (p > mx) mx = p;
-            }
-            gm += mx;
-        }
-        e += ldexp(gm + fabs(dot64(a, b, D)), -10);
-    }
-    return e;
+    const double n = (double)(D > 1 ? D - 1 : 0), u = ldexp(1.0, -24);
+    return n * u / (1.0 - n * u) * abs_dot64(a, b, D);
 }
 
-static uint64_t splitmix64(uint64_t x)
+/* The high-precision scores of one query row, keys 0 .. kmax (R15):
+ * acc[c] = fl32(q.k_c) from the fp64 dot product (exact: the fp64 value
+ * itself), or given[c] when the caller supplies the dot products; with eps
+ * set, eps[c] = the accumulation error bound of key c in S units. */
+static void row_scores(const attn_job* J, const uint16_t* qr, const uint16_t* kb, int kmax,
+                       const float* given, int exact, double* acc, double* eps)
 {
-    x += 0x9E3779B97F4A7C15ull;
-    x = (x ^ (x >> 30)) * 0xBF58476D1CE4E5B9ull;
-    x = (x ^ (x >> 27)) * 0x94D049BB133111EBull;
-    return x ^ (x >> 31);
+    const int D = J->D;
+    for (int c = 0; c <= kmax; ++c) {
+        const uint16_t* kr = kb + (int64_t)c * D;
+        if (given) acc[c] = (double)given[c];
+        else {
+            const double a = dot64(qr, kr, D);
+            acc[c] = exact ? a : (double)(float)a;
+        }
+        if (eps) eps[c] = acc_err(qr, kr, D) * J->c64;
+    }
 }
 
 /* Distance from x to the nearest point where the HiF8 rounding of x changes. */
@@ -503,8 +534,8 @@ typedef struct { double *acc, *eps, *ot, *pv, *ref, *bmargin; } row_scratch;
  * maximum, the restart test of every B1 block, and the ceil of the row
  * maximum of every block that takes the high-precision path.  A margin of
  * at least 1 means every valid high-precision S gives this same result. */
-static void row_alg1(const attn_job* J, int b, int h, int r, row_scratch* W,
-                     double* o, double* lse, int32_t* nrs, double* margin_out)
+static void row_alg1(const attn_job* J, int b, int h, int r, row_scratch* W, const float* given,
+                     double* o, double* lse, int32_t* nrs, double* margin_out, double* refs_out)
 {
     const int D = J->D, blk = J->block;
     const int g = h / (J->Hq / J->Hkv);                                   /* R17 */
@@ -514,24 +545,13 @@ static void row_alg1(const attn_job* J, int b, int h, int r, row_scratch* W,
     const int exact = (J->mode == ORC_E2E_EXACT);
     const int kmax = last_visible_key(J, r);
     const int nblk = kmax < 0 ? 0 : kmax / blk + 1;
-    const uint64_t rowid = (((uint64_t)b * J->Hq + h) * J->Sq + r);
+    const int want_margin = margin_out != NULL;
     double m = -INFINITY, d = 0.0;
     int32_t restarts = 0;
     for (int i = 0; i < D; ++i) W->ot[i] = 0.0;
 
     /* S = Q K^T * log2(e)/sqrt(d): keep acc, the unscaled dot product */
-    for (int c = 0; c <= kmax; ++c) {
-        const uint16_t* kr = kb + (int64_t)c * D;
-        double a = dot64(qr, kr, D);
-        const double e_acc = acc_err(J, qr, kr, D);
-        if (J->jitter != 0.0) {
-            double sgn = 1.0;
-            if (J->jitter_seed) sgn = (splitmix64(J->jitter_seed ^ (rowid * 1000003ull + (uint64_t)c)) & 1) ? 1.0 : -1.0;
-            a += J->jitter * sgn * e_acc;
-        }
-        W->acc[c] = exact ? a : (double)(float)a;
-        W->eps[c] = e_acc * J->c64;                                      /* in S units */
-    }
+    row_scores(J, qr, kb, kmax, given, exact, W->acc, want_margin ? W->eps : NULL);
 
     for (int j = 0; j < nblk; ++j) {
         const int c0 = j * blk;
@@ -540,7 +560,7 @@ static void row_alg1(const attn_job* J, int b, int h, int r, row_scratch* W,
         const int nc = c1 - c0;
         double bm = INFINITY, eps_blk = 0.0, amax = -INFINITY;
         for (int c = 0; c < nc; ++c) {
-            if (W->eps[c0 + c] > eps_blk) eps_blk = W->eps[c0 + c];
+            if (want_margin && W->eps[c0 + c] > eps_blk) eps_blk = W->eps[c0 + c];
             if (acc[c] > amax) amax = acc[c];
         }
         int restart;
@@ -554,11 +574,11 @@ static void row_alg1(const attn_job* J, int b, int h, int r, row_scratch* W,
             for (int c = 0; c < nc; ++c) {
                 double t;
                 if (exact) t = acc[c] * J->c64 - m;
-                else t = orc_hif8_round((double)fmaf((float)acc[c], J->c32, (float)(-m)), 1);
+                else t = orc_hif8_round((double)fmaf((float)acc[c], J->c32, (float)(-m)), J->hif8_flags);
                 if (t > tmax) tmax = t;
             }
             restart = ceil(tmax) > (double)J->lambda;
-            if (m != -INFINITY) {
+            if (want_margin && m != -INFINITY) {
                 double x = amax * J->c64 - m;
                 double dist = hif8_boundary_distance(x) / eps_blk;
                 if (dist < bm) bm = dist;
@@ -579,8 +599,10 @@ static void row_alg1(const attn_job* J, int b, int h, int r, row_scratch* W,
             }
             m_new = fmax(m, ceil(M));
             ref = m_new;
-            double dist = integer_distance(amax * J->c64) / eps_blk;
-            if (dist < bm) bm = dist;
+            if (want_margin) {
+                double dist = integer_distance(amax * J->c64) / eps_blk;
+                if (dist < bm) bm = dist;
+            }
         }
         /* P = 2^T in 8-bit, T = S - rowfill(m~) in 8-bit (eq. 3) */
         double rowsum = 0.0;
@@ -589,7 +611,7 @@ static void row_alg1(const attn_job* J, int b, int h, int r, row_scratch* W,
             double p;
             if (exact) p = exp2(acc[c] * J->c64 - ref);
             else {
-                double t = orc_hif8_round((double)fmaf((float)acc[c], J->c32, (float)(-ref)), 1);
+                double t = orc_hif8_round((double)fmaf((float)acc[c], J->c32, (float)(-ref)), J->hif8_flags);
                 p = e8_hif8(t);
             }
             if (p == 0.0) continue;
@@ -605,6 +627,7 @@ static void row_alg1(const attn_job* J, int b, int h, int r, row_scratch* W,
         m = m_new;
         W->ref[j] = ref;
         W->bmargin[j] = bm;
+        if (refs_out) refs_out[j] = ref;
     }
     if (margin_out) {
         double mg = INFINITY;
@@ -615,7 +638,8 @@ static void row_alg1(const attn_job* J, int b, int h, int r, row_scratch* W,
                 const int c1 = (c0 + blk <= kmax + 1) ? c0 + blk : kmax + 1;
                 for (int c = c0; c < c1; ++c) {
                     double x = W->acc[c] * J->c64 - W->ref[j];
-                    double p = e8_hif8(orc_hif8_round((double)fmaf((float)W->acc[c], J->c32, (float)(-W->ref[j])), 1));
+                    double p = e8_hif8(orc_hif8_round((double)fmaf((float)W->acc[c], J->c32, (float)(-W->ref[j])),
+                                                      J->hif8_flags));
                     if (ldexp(p, (int)(W->ref[j] - m)) < 1.0 / 4096.0) continue;
                     double dist = hif8_boundary_distance(x) / W->eps[c];
                     if (dist < mg) mg = dist;
@@ -648,8 +672,8 @@ static float round_bf16(float p)
     return p;
 }
 
-static void row_eq2(const attn_job* J, int b, int h, int r, row_scratch* W, double* o, double* lse,
-                    double* margin_out)
+static void row_eq2(const attn_job* J, int b, int h, int r, row_scratch* W, const float* given, double* o,
+                    double* lse, double* margin_out, double* refs_out)
 {
     const int D = J->D, blk = J->block;
     const int g = h / (J->Hq / J->Hkv);
@@ -658,8 +682,10 @@ static void row_eq2(const attn_job* J, int b, int h, int r, row_scratch* W, doub
     const uint16_t* vb = J->v + ((int64_t)b * J->Hkv + g) * (int64_t)J->Sk * D;
     const int kmax = last_visible_key(J, r);
     const int nblk = kmax < 0 ? 0 : kmax / blk + 1;
-    const uint64_t rowid = (((uint64_t)b * J->Hq + h) * J->Sq + r);
-    const orc_format *fin = &F_HIF8, *fout = &F_HIF8;
+    const int want_margin = margin_out != NULL;
+    /* (2^x of an 8-bit x is irrational or an exact power of two, never halfway
+     * between two HiF8 values: the output cast needs no tie rule) */
+    const orc_format *fin = hif8_fmt(J->hif8_flags), *fout = &F_HIF8;
     if (J->mode == ORC_EXP2_E4M3) { fin = &F_E4M3; fout = &F_E4M3; }
     if (J->mode == ORC_EXP2_E5M2) { fin = &F_E5M2; fout = &F_E5M2; }
     if (J->mode == ORC_EXP2_E4M3xE5M2) { fin = &F_E4M3; fout = &F_E5M2; }
@@ -678,21 +704,13 @@ static void row_eq2(const attn_job* J, int b, int h, int r, row_scratch* W, doub
         const int nc = c1 - c0;
         float rowmax = -INFINITY;
         double eps_rowmax = 0.0;
+        row_scores(J, qr, kb + (int64_t)c0 * D, nc - 1, given ? given + c0 : NULL, 0, W->acc,
+                   want_margin ? W->eps : NULL);
         for (int c = 0; c < nc; ++c) {
-            const uint16_t* kr = kb + (int64_t)(c0 + c) * D;
-            double a = dot64(qr, kr, D);
-            const double e_acc = acc_err(J, qr, kr, D);
-            if (J->jitter != 0.0) {
-                double sgn = 1.0;
-                if (J->jitter_seed)
-                    sgn = (splitmix64(J->jitter_seed ^ (rowid * 1000003ull + (uint64_t)(c0 + c))) & 1) ? 1.0 : -1.0;
-                a += J->jitter * sgn * e_acc;
-            }
-            float s = (float)a * J->c32;                                 /* S = fl32(fl32(q.k) * c) */
-            if (J->mode == ORC_NAIVE_E2E) s = (float)fmt_round(&F_HIF8, s, 1);   /* scores cast first */
+            float s = (float)W->acc[c] * J->c32;                         /* S = fl32(fl32(q.k) * c) */
+            if (J->mode == ORC_NAIVE_E2E) s = (float)fmt_round(fin, s, 1);       /* scores cast first */
             W->acc[c] = s;
-            W->eps[c] = e_acc * J->c64;
-            if (s > rowmax) { rowmax = s; eps_rowmax = W->eps[c]; }
+            if (s > rowmax) { rowmax = s; eps_rowmax = want_margin ? W->eps[c] : 0.0; }
         }
         const float m_new = m > rowmax ? m : rowmax;                     /* m^(j) */
         const double eps_new = m > rowmax ? eps_m : eps_rowmax;
@@ -702,7 +720,7 @@ static void row_eq2(const attn_job* J, int b, int h, int r, row_scratch* W, doub
         else {
             const float x = m - m_new;
             alpha = (float)fmt_round(fout, exp2(fmt_round(fin, (double)x, 1)), 1);
-            if (hif8_dec && m_new != m) {
+            if (want_margin && hif8_dec && m_new != m) {
                 const double dist = hif8_boundary_distance((double)x) / (eps_m + eps_new);
                 if (dist < mg) mg = dist;
             }
@@ -718,7 +736,7 @@ static void row_eq2(const attn_job* J, int b, int h, int r, row_scratch* W, doub
                 p = (float)fmt_round(fout, exp2(fmt_round(fin, (double)x, 1)), 1);
                 /* a score carrying weight >= 2^-12 of the block maximum's whose
                  * rounding sits near a boundary */
-                if (hif8_dec && x > -12.0f && W->acc[c] != m_new) {
+                if (want_margin && hif8_dec && x > -12.0f && W->acc[c] != m_new) {
                     const double dist = hif8_boundary_distance((double)x) / (W->eps[c] + eps_new);
                     if (dist < mg) mg = dist;
                 }
@@ -726,7 +744,7 @@ static void row_eq2(const attn_job* J, int b, int h, int r, row_scratch* W, doub
             /* with pv_bf16, the bf16 rounding of a weighted P is a decision too:
              * its distance to the nearest bf16 midpoint against the change of
              * P that the score error bounds allow (and a few ulps of exp2) */
-            if (J->pv_bf16 && J->mode == ORC_DEFAULT && x > -12.0f && p > 0.0f) {
+            if (want_margin && J->pv_bf16 && J->mode == ORC_DEFAULT && x > -12.0f && p > 0.0f) {
                 uint32_t u;
                 memcpy(&u, &p, 4);
                 const uint32_t mu = (u & 0xFFFF0000u) | 0x8000u;
@@ -744,6 +762,7 @@ static void row_eq2(const attn_job* J, int b, int h, int r, row_scratch* W, doub
         d += rowsum;
         m = m_new;
         eps_m = eps_new;
+        if (refs_out) refs_out[j] = (double)m;
     }
     if (margin_out) *margin_out = mg;
     if (nblk == 0) {
@@ -811,11 +830,13 @@ static void attn_range(void* p, int64_t i0, int64_t i1)
         int b = (int)(g / ((int64_t)J->Sq * J->Hq));
         double* o = J->o + i * D;
         double* lse = J->lse + i;
+        const float* given = J->acc_in ? J->acc_in + i * J->ld_acc : NULL;
+        double* refs = J->ref_out ? J->ref_out + i * J->ld_ref : NULL;
+        double* mg = J->margin ? J->margin + i : NULL;
         if (C->which) row_exact(J, b, h, r, &W, o, lse);
         else if (J->mode == ORC_E2E_HIF8 || J->mode == ORC_E2E_EXACT)
-            row_alg1(J, b, h, r, &W, o, lse, J->nrestart ? J->nrestart + i : NULL,
-                     J->margin ? J->margin + i : NULL);
-        else row_eq2(J, b, h, r, &W, o, lse, J->margin ? J->margin + i : NULL);
+            row_alg1(J, b, h, r, &W, given, o, lse, J->nrestart ? J->nrestart + i : NULL, mg, refs);
+        else row_eq2(J, b, h, r, &W, given, o, lse, mg, refs);
     }
     free(W.acc); free(W.eps); free(W.ot); free(W.pv); free(W.ref); free(W.bmargin);
 }
@@ -827,24 +848,48 @@ static int attn_check(int B, int Hq, int Hkv, int Sq, int Sk, int D, int block)
     return 0;
 }
 
+/* Shared set-up of the attention entry points. */
+static void job_init(attn_job* J, const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                     int B, int Hq, int Hkv, int Sq, int Sk, int D, int causal, int block,
+                     int mode, int lambda, int n_b0, int literal_else, double scale_log2,
+                     const int64_t* rows, double* o, double* lse, int32_t* nrestart, double* margin)
+{
+    memset(J, 0, sizeof(*J));
+    J->q = q; J->k = k; J->v = v;
+    J->B = B; J->Hq = Hq; J->Hkv = Hkv; J->Sq = Sq; J->Sk = Sk; J->D = D;
+    J->causal = causal; J->block = block;
+    J->mode = mode; J->lambda = lambda; J->n_b0 = n_b0; J->literal_else = literal_else;
+    J->rows = rows; J->o = o; J->lse = lse; J->nrestart = nrestart; J->margin = margin;
+    J->hif8_flags = ORC_SAT;
+    J->c64 = scale_log2 != 0.0 ? scale_log2 : M_LOG2E / sqrt((double)D);
+    J->c32 = (float)J->c64;
+    if (mode != ORC_E2E_EXACT) J->c64 = (double)J->c32;
+}
+
 /* rows: global query-row indices (b*Hq + h)*Sq + r; outputs o[nrows*D], lse[nrows].
  * scale_log2 = 0 selects log2(e)/sqrt(D).  margin (nullable): per-row decision
- * margin of the E2E HiF8 setup (see row_alg1).  jitter / jitter_seed move every
- * dot product by jitter times its accumulation error bound (all the same way
- * for seed 0, random signs otherwise): another valid high-precision S.
- * Returns 0 or 1 (bad arguments). */
+ * margin (see row_alg1).  tie_even: the 8-bit casts of T (Alg. 1) and x (Exp2
+ * HiF8) round ties to even.  acc_in (nullable): the high-precision dot
+ * products of requested row i at acc_in[i*ld_acc + c] for every key c the row
+ * sees (another valid S of R15, e.g. a matrix unit's own sums).  ref_out
+ * (nullable): per requested row i and visible key block j, the reference at
+ * ref_out[i*ld_ref + j] (entries of blocks the row does not see are left as
+ * they are).  Returns 0 or 1 (bad arguments). */
 int orc_attention_ex(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                      int B, int Hq, int Hkv, int Sq, int Sk, int D, int causal, int block,
                      int mode, int lambda, int n_b0, int literal_else, double scale_log2,
                      const int64_t* rows, int64_t nrows, double* o, double* lse, int32_t* nrestart,
-                     double* margin, double jitter, uint64_t jitter_seed, int nthreads, int pv_bf16, int qk_fp8)
+                     double* margin, int nthreads, int pv_bf16, int tie_even,
+                     const float* acc_in, int64_t ld_acc, double* ref_out, int64_t ld_ref)
 {
     if (attn_check(B, Hq, Hkv, Sq, Sk, D, block) || mode < 0 || mode > 7) return 1;
-    attn_job J = { q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, block, mode, lambda, n_b0,
-                   literal_else, 0.0f, 0.0, rows, o, lse, nrestart, margin, jitter, jitter_seed, pv_bf16, qk_fp8 };
-    J.c64 = scale_log2 != 0.0 ? scale_log2 : M_LOG2E / sqrt((double)D);
-    J.c32 = (float)J.c64;
-    if (mode != ORC_E2E_EXACT) J.c64 = (double)J.c32;
+    if ((acc_in && ld_acc < Sk) || (ref_out && ld_ref < (Sk + block - 1) / block)) return 1;
+    attn_job J;
+    job_init(&J, q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, block, mode, lambda, n_b0, literal_else,
+             scale_log2, rows, o, lse, nrestart, margin);
+    J.pv_bf16 = pv_bf16;
+    J.hif8_flags = ORC_SAT | (tie_even ? ORC_EVEN : 0);
+    J.acc_in = acc_in; J.ld_acc = ld_acc; J.ref_out = ref_out; J.ld_ref = ld_ref;
     attn_ctx C = { &J, 0 };
     parallel_for(nrows, nthreads, 1, attn_range, &C);
     return 0;
@@ -857,8 +902,8 @@ int orc_attention(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                   int nthreads)
 {
     return orc_attention_ex(q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, block, mode, lambda, n_b0,
-                            literal_else, scale_log2, rows, nrows, o, lse, nrestart, NULL, 0.0, 0,
-                            nthreads, 0, 0);
+                            literal_else, scale_log2, rows, nrows, o, lse, nrestart, NULL, nthreads, 0, 0,
+                            NULL, 0, NULL, 0);
 }
 
 /* ------------------------------------------------------------------------ */
@@ -888,7 +933,8 @@ typedef struct {
 } tile_scratch;
 
 static void tile_alg1(const attn_job* J, int b0_last, int b, int h, int r0, int nr, tile_scratch* T,
-                      double* o, double* lse, int32_t* nrs, int32_t* nvis, double* margin)
+                      const float* const* given, double* o, double* lse, int32_t* nrs, int32_t* nvis,
+                      double* margin)
 {
     const int D = J->D, blk = J->block;
     const int g = h / (J->Hq / J->Hkv);
@@ -899,7 +945,6 @@ static void tile_alg1(const attn_job* J, int b0_last, int b, int h, int r0, int 
     for (int i = 0; i < nr; ++i) {
         const int r = r0 + i;
         const uint16_t* qr = J->q + (((int64_t)b * J->Hq + h) * J->Sq + r) * D;
-        const uint64_t rowid = (((uint64_t)b * J->Hq + h) * J->Sq + r);
         T->kmax[i] = last_visible_key(J, r);
         T->nblk[i] = T->kmax[i] < 0 ? 0 : T->kmax[i] / blk + 1;
         if (T->nblk[i] > nblk_t) nblk_t = T->nblk[i];
@@ -907,19 +952,7 @@ static void tile_alg1(const attn_job* J, int b0_last, int b, int h, int r0, int 
         T->d[i] = 0.0;
         T->mg[i] = INFINITY;
         for (int x = 0; x < D; ++x) T->ot[i][x] = 0.0;
-        for (int c = 0; c <= T->kmax[i]; ++c) {                          /* as in row_alg1 */
-            const uint16_t* kr = kb + (int64_t)c * D;
-            double a = dot64(qr, kr, D);
-            const double e_acc = acc_err(J, qr, kr, D);
-            if (J->jitter != 0.0) {
-                double sgn = 1.0;
-                if (J->jitter_seed)
-                    sgn = (splitmix64(J->jitter_seed ^ (rowid * 1000003ull + (uint64_t)c)) & 1) ? 1.0 : -1.0;
-                a += J->jitter * sgn * e_acc;
-            }
-            T->acc[i][c] = exact ? a : (double)(float)a;
-            T->eps[i][c] = e_acc * J->c64;
-        }
+        row_scores(J, qr, kb, T->kmax[i], given ? given[i] : NULL, exact, T->acc[i], margin ? T->eps[i] : NULL);
     }
     int32_t t_restart = 0, t_visit = 0;
     double tile_mg = INFINITY;
@@ -934,10 +967,10 @@ static void tile_alg1(const attn_job* J, int b0_last, int b, int h, int r0, int 
             double amax = -INFINITY, eb = 0.0, tmax = -INFINITY;
             for (int c = c0; c < c1; ++c) {
                 if (T->acc[i][c] > amax) amax = T->acc[i][c];
-                if (T->eps[i][c] > eb) eb = T->eps[i][c];
+                if (margin && T->eps[i][c] > eb) eb = T->eps[i][c];
                 double t;
                 if (exact) t = T->acc[i][c] * J->c64 - T->m[i];
-                else t = orc_hif8_round((double)fmaf((float)T->acc[i][c], J->c32, (float)(-T->m[i])), 1);
+                else t = orc_hif8_round((double)fmaf((float)T->acc[i][c], J->c32, (float)(-T->m[i])), J->hif8_flags);
                 if (t > tmax) tmax = t;
             }
             T->amax[i] = amax;
@@ -949,7 +982,7 @@ static void tile_alg1(const attn_job* J, int b0_last, int b, int h, int r0, int 
                 restart = 1;
             } else {
                 if (ceil(tmax) > (double)J->lambda) restart = 1;
-                if (T->m[i] != -INFINITY) {
+                if (margin && T->m[i] != -INFINITY) {
                     double dist = hif8_boundary_distance(amax * J->c64 - T->m[i]) / eb;
                     if (dist < tile_mg) tile_mg = dist;
                 }
@@ -973,8 +1006,10 @@ static void tile_alg1(const attn_job* J, int b0_last, int b, int h, int r0, int 
                 }
                 m_new = fmax(m, ceil(M));
                 ref = m_new;
-                double dist = integer_distance(T->amax[i] * J->c64) / T->eps_blk[i];
-                if (dist < tile_mg) tile_mg = dist;
+                if (margin) {
+                    double dist = integer_distance(T->amax[i] * J->c64) / T->eps_blk[i];
+                    if (dist < tile_mg) tile_mg = dist;
+                }
             } else {
                 m_new = m + fmax(0.0, ceil(T->tmax[i]));
                 ref = m;
@@ -984,7 +1019,7 @@ static void tile_alg1(const attn_job* J, int b0_last, int b, int h, int r0, int 
             for (int c = c0; c < c1; ++c) {
                 double p;
                 if (exact) p = exp2(T->acc[i][c] * J->c64 - ref);
-                else p = e8_hif8(orc_hif8_round((double)fmaf((float)T->acc[i][c], J->c32, (float)(-ref)), 1));
+                else p = e8_hif8(orc_hif8_round((double)fmaf((float)T->acc[i][c], J->c32, (float)(-ref)), J->hif8_flags));
                 if (p == 0.0) continue;
                 rowsum += p;
                 const uint16_t* vr = vb + (int64_t)c * D;
@@ -1006,7 +1041,7 @@ static void tile_alg1(const attn_job* J, int b0_last, int b, int h, int r0, int 
                 for (int c = c0; c < c1; ++c) {
                     double x = T->acc[i][c] * J->c64 - T->ref[i][j];
                     double p = e8_hif8(orc_hif8_round((double)fmaf((float)T->acc[i][c], J->c32,
-                                                                   (float)(-T->ref[i][j])), 1));
+                                                                   (float)(-T->ref[i][j])), J->hif8_flags));
                     if (ldexp(p, (int)(T->ref[i][j] - T->m[i])) < 1.0 / 4096.0) continue;
                     double dist = hif8_boundary_distance(x) / T->eps[i][c];
                     if (dist < tile_mg) tile_mg = dist;
@@ -1064,6 +1099,7 @@ static void tiles_range(void* p, int64_t t0, int64_t t1)
     double* mg = (double*)malloc(sizeof(double) * R);
     int32_t* nrs = (int32_t*)malloc(sizeof(int32_t) * R);
     int32_t* nvs = (int32_t*)malloc(sizeof(int32_t) * R);
+    const float** given = (const float**)malloc(sizeof(float*) * R);
     for (int64_t t = t0; t < t1; ++t) {
         const int64_t key = C->tiles[t];
         const int tq = (int)(key % ntq);
@@ -1071,7 +1107,20 @@ static void tiles_range(void* p, int64_t t0, int64_t t1)
         const int b = (int)(key / (ntq * J->Hq));
         const int r0 = tq * R;
         const int nr = (r0 + R <= J->Sq) ? R : J->Sq - r0;
-        tile_alg1(J, C->b0_last, b, h, r0, nr, &T, o, lse, nrs, nvs, J->margin ? mg : NULL);
+        if (J->acc_in) {
+            /* supplied dot products: every row of the tile takes part in its
+             * decisions, so every row of the tile must have been requested */
+            for (int i = 0; i < nr; ++i) given[i] = NULL;
+            for (int64_t e = C->first[t]; e < C->first[t + 1]; ++e) {
+                const int64_t i = C->order[e];
+                given[(int)(J->rows[i] % J->Sq) - r0] = J->acc_in + i * J->ld_acc;
+            }
+            int missing = 0;
+            for (int i = 0; i < nr; ++i) missing |= given[i] == NULL;
+            if (missing) { __atomic_store_n(&J->err, 1, __ATOMIC_RELAXED); continue; }
+        }
+        tile_alg1(J, C->b0_last, b, h, r0, nr, &T, J->acc_in ? given : NULL, o, lse, nrs, nvs,
+                  J->margin ? mg : NULL);
         for (int64_t e = C->first[t]; e < C->first[t + 1]; ++e) {
             const int64_t i = C->order[e];
             const int r = (int)(J->rows[i] % J->Sq) - r0;
@@ -1080,8 +1129,11 @@ static void tiles_range(void* p, int64_t t0, int64_t t1)
             if (J->nrestart) J->nrestart[i] = nrs[r];
             if (C->nvisit) C->nvisit[i] = nvs[r];
             if (J->margin) J->margin[i] = mg[r];
+            if (J->ref_out)
+                for (int j = 0; j < T.nblk[r]; ++j) J->ref_out[i * J->ld_ref + j] = T.ref[r][j];
         }
     }
+    free(given);
     for (int i = 0; i < R; ++i) { free(T.acc[i]); free(T.eps[i]); free(T.ot[i]); free(T.pv[i]); free(T.ref[i]); }
     free(T.acc); free(T.eps); free(T.ot); free(T.pv); free(T.ref);
     free(T.m); free(T.d); free(T.tmax); free(T.amax); free(T.eps_blk); free(T.mg); free(T.kmax); free(T.nblk);
@@ -1104,16 +1156,17 @@ int orc_attention_tiles(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                         int B, int Hq, int Hkv, int Sq, int Sk, int D, int causal, int block,
                         int mode, int lambda, int n_b0, int b0_last, int restart_rows, int literal_else,
                         double scale_log2, const int64_t* rows, int64_t nrows, double* o, double* lse,
-                        int32_t* nrestart, int32_t* nvisit, double* margin, double jitter,
-                        uint64_t jitter_seed, int nthreads, int qk_fp8)
+                        int32_t* nrestart, int32_t* nvisit, double* margin, int nthreads, int tie_even,
+                        const float* acc_in, int64_t ld_acc, double* ref_out, int64_t ld_ref)
 {
     if (attn_check(B, Hq, Hkv, Sq, Sk, D, block)) return 1;
     if ((mode != ORC_E2E_HIF8 && mode != ORC_E2E_EXACT) || restart_rows < 1 || n_b0 < 0) return 1;
-    attn_job J = { q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, block, mode, lambda, n_b0,
-                   literal_else, 0.0f, 0.0, rows, o, lse, nrestart, margin, jitter, jitter_seed, 0, qk_fp8 };
-    J.c64 = scale_log2 != 0.0 ? scale_log2 : M_LOG2E / sqrt((double)D);
-    J.c32 = (float)J.c64;
-    if (mode != ORC_E2E_EXACT) J.c64 = (double)J.c32;
+    if ((acc_in && ld_acc < Sk) || (ref_out && ld_ref < (Sk + block - 1) / block)) return 1;
+    attn_job J;
+    job_init(&J, q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, block, mode, lambda, n_b0, literal_else,
+             scale_log2, rows, o, lse, nrestart, margin);
+    J.hif8_flags = ORC_SAT | (tie_even ? ORC_EVEN : 0);
+    J.acc_in = acc_in; J.ld_acc = ld_acc; J.ref_out = ref_out; J.ld_ref = ld_ref;
     if (nrows == 0) return 0;
     const int R = restart_rows;
     const int64_t ntq = (Sq + R - 1) / R;
@@ -1140,7 +1193,7 @@ int orc_attention_tiles(const uint16_t* q, const uint16_t* k, const uint16_t* v,
     tiles_ctx C = { &J, R, b0_last ? 1 : 0, tiles, first, order, nvisit };
     parallel_for(nt, nthreads, 1, tiles_range, &C);
     free(key); free(order); free(tiles); free(first);
-    return 0;
+    return J.err ? 1 : 0;
 }
 
 int orc_exact_attention(const uint16_t* q, const uint16_t* k, const uint16_t* v,
@@ -1149,9 +1202,9 @@ int orc_exact_attention(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                         double* o, double* lse, int nthreads)
 {
     if (attn_check(B, Hq, Hkv, Sq, Sk, D, 1)) return 1;
-    attn_job J = { q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, 1, 0, 0, 0, 0, 0.0f, 0.0,
-                   rows, o, lse, NULL, NULL, 0.0, 0 };
-    J.c64 = scale_log2 != 0.0 ? scale_log2 : M_LOG2E / sqrt((double)D);
+    attn_job J;
+    job_init(&J, q, k, v, B, Hq, Hkv, Sq, Sk, D, causal, 1, ORC_E2E_EXACT, 0, 0, 0, scale_log2, rows, o, lse,
+             NULL, NULL);
     attn_ctx C = { &J, 1 };
     parallel_for(nrows, nthreads, 1, attn_range, &C);
     return 0;

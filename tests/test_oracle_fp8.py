@@ -92,21 +92,3 @@ def test_fp8_scale_folds_into_the_score_scale():
     # scales without changing it
     assert O.fp8_scale_log2(128, 0.25, 4.0) == O.fp8_scale_log2(128, 1.0, 1.0) == math.log2(math.e) / math.sqrt(128)
     assert O.fp8_scale_log2(64, 0.5, 0.5, scale_log2=2.0) == 0.5
-
-
-def test_fp8_bound_only_widens_the_margins():
-    # the FP8 matrix unit's accumulation bound is wider than the fp32 one: the
-    # same result, margins no larger, and a jitter of the wider bound moves
-    # the result of some row
-    from paper_2602_02071_amd.workloads import make_qk_fp8, make_qkv
-    q, k, v = make_qkv(1, 2, 1, 32, 256, 128, seed=4, outliers=True)
-    q8, k8, qs, ks = make_qk_fp8(q, k)
-    qb, kb = O.e4m3_to_bf16(q8), O.e4m3_to_bf16(k8)
-    c = O.fp8_scale_log2(128, qs, ks)
-    args = (qb, kb, v, 1, 2, 1, 32, 256, 128, True, 64)
-    o1, l1, _, m1 = O.attention(*args, scale_log2=c, margin=True)
-    o2, l2, _, m2 = O.attention(*args, scale_log2=c, margin=True, qk_fp8=True)
-    assert np.array_equal(o1, o2) and np.array_equal(l1, l2)
-    assert np.all(m2 <= m1) and np.any(m2 < m1)
-    oj, _, _ = O.attention(*args, scale_log2=c, qk_fp8=True, jitter=1.0)
-    assert np.abs(oj - o1).max() > 0
