@@ -42,6 +42,7 @@ extern "C" {
 #define BAPS_HIP_ERROR 3
 
 #define BAPS_HIF8_SATURATE 1
+#define BAPS_HIF8_TIES_EVEN 2
 
 /*
  * Fused BAPS attention forward, canonical setup ("E2E HiF8", Sec. 4.1):
@@ -104,16 +105,59 @@ typedef struct {
                                             computed in the dequantisation).  Not with
                                             restart_rows > 1                                  */
     float q_scale, k_scale;              /* FP8 dequantisation scales (finite, > 0)            */
+    int tie_mode;                        /* the 8-bit cast of T (eq. 3): BAPS_TIES_AWAY (0,
+                                            canonical) or BAPS_TIES_EVEN (1, E2E setup with
+                                            lambda <= 8, restart_rows <= 1 and bf16 Q/K; else
+                                            BAPS_UNSUPPORTED); anything else is invalid       */
+    int saturate;                        /* nonzero: the 8-bit casts clamp finite overflow to
+                                            +-2^15 (canonical); 0: they round it to +-Inf.
+                                            Identical results unless an 8-bit P can exceed 2^15,
+                                            i.e. lambda >= 16 in the E2E setup, which is
+                                            BAPS_UNSUPPORTED with saturate = 0                */
+    int out_bf16;                        /* nonzero: o receives bf16 (each element the round-to-
+                                            nearest-even bf16 of the fp32 result) in place of
+                                            fp32: B*Hq*Sq*D 16-bit values at the same 16-byte
+                                            aligned address (the float* is reinterpreted)      */
 } baps_params_t;
 
 #define BAPS_QK_BF16 0
 #define BAPS_QK_FP8_E4M3 1
+#define BAPS_TIES_AWAY 0
+#define BAPS_TIES_EVEN 1
 
 /* baps_attention_fwd with explicit knobs; p must not be NULL; scale_log2
- * must be >= 0. */
+ * must be >= 0.  A caller that fills the struct by hand sets saturate = 1 for
+ * the canonical cast (0 is accepted and gives the same result below lambda 16). */
 int baps_attention_fwd_ex(const void* q, const void* k, const void* v, float* o, float* lse,
                           int B, int Hq, int Hkv, int Sq, int Sk, int D, int causal, int block,
                           const baps_params_t* p, void* stream);
+
+/*
+ * Verification entry point: baps_attention_fwd_ex (p may be NULL: canonical
+ * knobs) on the one-pass kernels of that call, built with a dump of the
+ * high-precision scores S that Alg. 1 computes "in high precision" (R15: the
+ * matrix unit's own fp32 sums q.k, before the scale) and of the reference of
+ * every key block, for the query rows the caller selects.  O, lse and every
+ * other output equal those of baps_attention_fwd_ex on the same arguments
+ * (the kernels differ only by the extra stores), so an independent
+ * implementation of Alg. 1 run on the dumped S must reproduce O bit for bit
+ * in its decisions and up to the order of fp32 additions in its sums.
+ *   row_slot [B*Hq*Sq] int32 (device): for query row (b*Hq + h)*Sq + r, -1
+ *            or a slot s in [0, nslots); distinct rows take distinct slots;
+ *   acc_out  [nslots][Sk] fp32 (device): acc_out[s*Sk + c] = q.k_c for every
+ *            key c the row sees (under the causal mask); other entries are
+ *            left as they are;
+ *   ref_out  [nslots][ceil(Sk/block)] fp32 (device): the reference after
+ *            every key block j the row sees (Alg. 1's integer m~ that T is
+ *            taken against; the running maximum m in the eq. (2) setups);
+ *            other entries are left as they are.
+ * The caller owns the buffers and sizes them for its nslots.  Status 1 when
+ * row_slot, or acc_out / ref_out with Sk > 0, is NULL.
+ */
+int baps_attention_fwd_dump(const void* q, const void* k, const void* v, float* o, float* lse,
+                            int B, int Hq, int Hkv, int Sq, int Sk, int D, int causal, int block,
+                            const baps_params_t* p, const int* row_slot, float* acc_out, float* ref_out,
+                            void* stream);
 
 /*
  * Split-key path for few query rows per key/value head (single-sequence or
@@ -149,10 +193,15 @@ int baps_attention_fwd_split(const void* q, const void* k, const void* v, float*
 /*
  * HiF8 codec (the 8-bit format used by every 8-bit step of the method;
  * Sec. 2, App. A).  hif8_encode: codes[i] = code of the HiF8 value nearest
- * to x[i] (ties away from zero).  flags: BAPS_HIF8_SATURATE clamps finite
- * overflow to +-2^15 (else values from 1.25*2^15 up become +-Inf); no other
- * bit may be set.  +-Inf -> 0x6F/0xEF, NaN -> 0x80, values that round to
- * zero -> 0x00.  hif8_decode: x[i] = value of codes[i] (0x80 -> NaN).
+ * to x[i].  flags: BAPS_HIF8_SATURATE clamps finite overflow to +-2^15 (else
+ * values from 1.25*2^15 up become +-Inf); BAPS_HIF8_TIES_EVEN sends a value
+ * exactly halfway between two HiF8 values to the one whose significand is
+ * even (an even multiple of their spacing: between the last value of a
+ * binade and the next power of two, and among the powers of two below
+ * 2^-15, that is the upper one; between 0 and 2^-22 it is 0; at the
+ * overflow midpoint it is 2^15), else ties go away from zero; no other bit
+ * may be set.  +-Inf -> 0x6F/0xEF, NaN -> 0x80, values that round to zero
+ * -> 0x00.  hif8_decode: x[i] = value of codes[i] (0x80 -> NaN).
  * n >= 0 elements; any alignment (16-byte aligned buffers stream faster).
  */
 int hif8_encode(const float* x, unsigned char* codes, long long n, int flags, void* stream);

@@ -18,9 +18,12 @@ BAPS_INVALID_ARGUMENT = 1
 BAPS_UNSUPPORTED = 2
 BAPS_HIP_ERROR = 3
 BAPS_HIF8_SATURATE = 1
+BAPS_HIF8_TIES_EVEN = 2
+BAPS_TIES_AWAY = 0
+BAPS_TIES_EVEN = 1
 
-EXPORTS = ("baps_attention_fwd", "baps_attention_fwd_ex", "baps_attention_fwd_split", "hif8_encode",
-           "hif8_decode", "baps_softmax_block", "baps_get_exp2_lut", "baps_init",
+EXPORTS = ("baps_attention_fwd", "baps_attention_fwd_ex", "baps_attention_fwd_split", "baps_attention_fwd_dump",
+           "hif8_encode", "hif8_decode", "baps_softmax_block", "baps_get_exp2_lut", "baps_init",
            "baps_attention_split_workspace", "baps_last_hip_error", "baps_status_string")
 
 _lib = None
@@ -37,7 +40,8 @@ class baps_params_t(ctypes.Structure):
     _fields_ = [("lambda_", ctypes.c_int), ("n_b0", ctypes.c_int), ("scale_log2", ctypes.c_float),
                 ("restart_counts", ctypes.c_void_p), ("mode", ctypes.c_int), ("restart_rows", ctypes.c_int),
                 ("b0_last", ctypes.c_int), ("tile_counts", ctypes.c_void_p), ("qk_format", ctypes.c_int),
-                ("q_scale", ctypes.c_float), ("k_scale", ctypes.c_float)]
+                ("q_scale", ctypes.c_float), ("k_scale", ctypes.c_float), ("tie_mode", ctypes.c_int),
+                ("saturate", ctypes.c_int), ("out_bf16", ctypes.c_int)]
 
 
 # softmax setups (include/baps.h)
@@ -68,6 +72,8 @@ def load():
                                         ctypes.POINTER(baps_params_t), P]
     L.baps_attention_fwd_split.argtypes = [P, P, P, P, P, I, I, I, I, I, I, I, I,
                                            ctypes.POINTER(baps_params_t), P, LL, P]
+    L.baps_attention_fwd_dump.argtypes = [P, P, P, P, P, I, I, I, I, I, I, I, I,
+                                          ctypes.POINTER(baps_params_t), P, P, P, P]
     L.baps_attention_split_workspace.argtypes = [I, I, I, I, I, I, I, ctypes.POINTER(baps_params_t)]
     L.hif8_encode.argtypes = [P, P, LL, I, P]
     L.hif8_decode.argtypes = [P, P, LL, P]
@@ -118,33 +124,51 @@ def baps_attention_fwd(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, st
 
 
 def _params(lam=1, n_b0=1, scale_log2=0.0, restart_counts=None, mode=BAPS_MODE_E2E_HIF8, restart_rows=1,
-            b0_last=False, tile_counts=None, qk_scales=None):
+            b0_last=False, tile_counts=None, qk_scales=None, tie_mode=BAPS_TIES_AWAY, saturate=True,
+            out_bf16=False):
     fmt, qs, ks = (BAPS_QK_BF16, 1.0, 1.0) if qk_scales is None else (BAPS_QK_FP8_E4M3,) + tuple(qk_scales)
     return baps_params_t(int(lam), int(n_b0), float(scale_log2), _p(restart_counts), int(mode), int(restart_rows),
-                         int(bool(b0_last)), _p(tile_counts), int(fmt), float(qs), float(ks))
+                         int(bool(b0_last)), _p(tile_counts), int(fmt), float(qs), float(ks), int(tie_mode),
+                         int(bool(saturate)), int(bool(out_bf16)))
 
 
 def baps_attention_fwd_ex(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, lam=1, n_b0=1,
                           scale_log2=0.0, restart_counts=None, stream=None, mode=BAPS_MODE_E2E_HIF8,
-                          restart_rows=1, b0_last=False, tile_counts=None, qk_scales=None):
-    """qk_scales=(q_scale, k_scale): q and k are FP8 E4M3 codes (uint8 tensors)."""
-    prm = _params(lam, n_b0, scale_log2, restart_counts, mode, restart_rows, b0_last, tile_counts, qk_scales)
+                          restart_rows=1, b0_last=False, tile_counts=None, qk_scales=None, tie_mode=BAPS_TIES_AWAY,
+                          saturate=True, out_bf16=False):
+    """qk_scales=(q_scale, k_scale): q and k are FP8 E4M3 codes (uint8 tensors).
+    out_bf16: o is a bf16 tensor."""
+    prm = _params(lam, n_b0, scale_log2, restart_counts, mode, restart_rows, b0_last, tile_counts, qk_scales,
+                  tie_mode, saturate, out_bf16)
     _check("baps_attention_fwd_ex", load().baps_attention_fwd_ex(
         _p(q), _p(k), _p(v), _p(o), _p(lse), B, Hq, Hkv, Sq, Sk, D, int(causal), block,
         ctypes.byref(prm), _stream(stream)))
 
 
+def baps_attention_fwd_dump(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, row_slot, acc_out, ref_out,
+                            stream=None, **knobs):
+    """The fused pass with a dump of the selected rows' raw dot products and
+    block references (include/baps.h); knobs as baps_attention_fwd_ex."""
+    prm = _params(**knobs)
+    _check("baps_attention_fwd_dump", load().baps_attention_fwd_dump(
+        _p(q), _p(k), _p(v), _p(o), _p(lse), B, Hq, Hkv, Sq, Sk, D, int(causal), block,
+        ctypes.byref(prm), _p(row_slot), _p(acc_out), _p(ref_out), _stream(stream)))
+
+
 def baps_attention_split_workspace(B, Hq, Hkv, Sq, Sk, D, block, lam=1, n_b0=1, scale_log2=0.0,
-                                   mode=BAPS_MODE_E2E_HIF8, restart_rows=1, b0_last=False, qk_scales=None):
-    prm = _params(lam, n_b0, scale_log2, None, mode, restart_rows, b0_last, None, qk_scales)
+                                   mode=BAPS_MODE_E2E_HIF8, restart_rows=1, b0_last=False, qk_scales=None,
+                                   tie_mode=BAPS_TIES_AWAY, saturate=True, out_bf16=False):
+    prm = _params(lam, n_b0, scale_log2, None, mode, restart_rows, b0_last, None, qk_scales, tie_mode, saturate,
+                  out_bf16)
     return int(load().baps_attention_split_workspace(B, Hq, Hkv, Sq, Sk, D, block, ctypes.byref(prm)))
 
 
 def baps_attention_fwd_split(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, workspace, workspace_bytes,
                              lam=1, n_b0=1, scale_log2=0.0, restart_counts=None, stream=None,
                              mode=BAPS_MODE_E2E_HIF8, restart_rows=1, b0_last=False, tile_counts=None,
-                             qk_scales=None):
-    prm = _params(lam, n_b0, scale_log2, restart_counts, mode, restart_rows, b0_last, tile_counts, qk_scales)
+                             qk_scales=None, tie_mode=BAPS_TIES_AWAY, saturate=True, out_bf16=False):
+    prm = _params(lam, n_b0, scale_log2, restart_counts, mode, restart_rows, b0_last, tile_counts, qk_scales,
+                  tie_mode, saturate, out_bf16)
     _check("baps_attention_fwd_split", load().baps_attention_fwd_split(
         _p(q), _p(k), _p(v), _p(o), _p(lse), B, Hq, Hkv, Sq, Sk, D, int(causal), block,
         ctypes.byref(prm), _p(workspace), int(workspace_bytes), _stream(stream)))
@@ -178,35 +202,73 @@ def baps_init():
 # ------------------------------------------------------------ tensor helpers
 def attention(q, k, v, causal, block, lse=True, lam=None, n_b0=None, scale_log2=0.0, restart_counts=None,
               stream=None, mode=BAPS_MODE_E2E_HIF8, split=False, restart_rows=1, b0_last=False, tile_counts=None,
-              qk_scales=None):
+              qk_scales=None, tie_mode=BAPS_TIES_AWAY, saturate=True, out_bf16=False):
     """Allocate O (and lse) with torch on q's device and run the fused pass.
     q [B,Hq,Sq,D], k/v [B,Hkv,Sk,D] bf16 CUDA tensors, contiguous.  split:
     take baps_attention_fwd_split, with a workspace allocated here.
     restart_rows / b0_last / tile_counts: the tile-level restart knobs of
     baps_params_t.  qk_scales=(q_scale, k_scale): q and k are FP8 E4M3 codes
-    (uint8 tensors) with those dequantisation scales."""
+    (uint8 tensors) with those dequantisation scales.  out_bf16: O is
+    returned as bf16."""
     import torch
     B, Hq, Sq, D = q.shape
     Hkv, Sk = k.shape[1], k.shape[2]
+    _check_inputs(q, k, v, qk_scales)
+    o = torch.empty((B, Hq, Sq, D), dtype=torch.bfloat16 if out_bf16 else torch.float32, device=q.device)
+    l = torch.empty((B, Hq, Sq), dtype=torch.float32, device=q.device) if lse else None
+    lam_, nb_ = 1 if lam is None else lam, 1 if n_b0 is None else n_b0
+    extra = dict(tie_mode=tie_mode, saturate=saturate, out_bf16=out_bf16)
+    if split:
+        nbytes = baps_attention_split_workspace(B, Hq, Hkv, Sq, Sk, D, block, lam_, nb_, scale_log2, mode,
+                                                restart_rows, b0_last, qk_scales, **extra)
+        ws = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=q.device)
+        baps_attention_fwd_split(q, k, v, o, l, B, Hq, Hkv, Sq, Sk, D, causal, block, ws, nbytes, lam_, nb_,
+                                 scale_log2, restart_counts, stream, mode, restart_rows, b0_last, tile_counts,
+                                 qk_scales, **extra)
+    elif (lam is None and n_b0 is None and not scale_log2 and restart_counts is None and mode == BAPS_MODE_E2E_HIF8
+          and restart_rows == 1 and not b0_last and tile_counts is None and qk_scales is None
+          and tie_mode == BAPS_TIES_AWAY and saturate and not out_bf16):
+        baps_attention_fwd(q, k, v, o, l, B, Hq, Hkv, Sq, Sk, D, causal, block, stream)
+    else:
+        baps_attention_fwd_ex(q, k, v, o, l, B, Hq, Hkv, Sq, Sk, D, causal, block, lam_, nb_, scale_log2,
+                              restart_counts, stream, mode, restart_rows, b0_last, tile_counts, qk_scales, **extra)
+    return o, l
+
+
+def _check_inputs(q, k, v, qk_scales):
+    import torch
     qk_dtype = torch.bfloat16 if qk_scales is None else torch.uint8
     for t, dt in ((q, qk_dtype), (k, qk_dtype), (v, torch.bfloat16)):
         if t.dtype != dt or not t.is_contiguous() or not t.is_cuda:
             raise ValueError("q, k (bf16, or uint8 FP8 codes with qk_scales) and v (bf16) must be contiguous "
                              "device tensors")
+
+
+def attention_dump(q, k, v, causal, block, rows, lam=1, n_b0=1, scale_log2=0.0, mode=BAPS_MODE_E2E_HIF8,
+                   restart_rows=1, b0_last=False, qk_scales=None, tie_mode=BAPS_TIES_AWAY, saturate=True,
+                   stream=None):
+    """baps_attention_fwd_dump with buffers allocated here: the fused pass
+    (o, lse as from attention()) plus, for the global query rows `rows`
+    ((b*Hq + h)*Sq + r, distinct), their raw dot products acc [n, Sk] (NaN
+    where the row sees no key) and block references ref [n, ceil(Sk/block)]
+    (NaN where the row sees no key of the block), as device tensors."""
+    import torch
+    B, Hq, Sq, D = q.shape
+    Hkv, Sk = k.shape[1], k.shape[2]
+    _check_inputs(q, k, v, qk_scales)
+    rows = torch.as_tensor(rows, dtype=torch.int64).reshape(-1)
+    n = rows.numel()
+    if n and (rows.min() < 0 or rows.max() >= B * Hq * Sq or rows.unique().numel() != n):
+        raise ValueError("rows must be distinct query-row indices")
+    slot = torch.full((B * Hq * Sq,), -1, dtype=torch.int32)
+    slot[rows] = torch.arange(n, dtype=torch.int32)
+    slot = slot.to(q.device)
+    nblk = (Sk + block - 1) // block
+    acc = torch.full((max(n, 1), max(Sk, 1)), float("nan"), dtype=torch.float32, device=q.device)
+    ref = torch.full((max(n, 1), max(nblk, 1)), float("nan"), dtype=torch.float32, device=q.device)
     o = torch.empty((B, Hq, Sq, D), dtype=torch.float32, device=q.device)
-    l = torch.empty((B, Hq, Sq), dtype=torch.float32, device=q.device) if lse else None
-    lam_, nb_ = 1 if lam is None else lam, 1 if n_b0 is None else n_b0
-    if split:
-        nbytes = baps_attention_split_workspace(B, Hq, Hkv, Sq, Sk, D, block, lam_, nb_, scale_log2, mode,
-                                                restart_rows, b0_last, qk_scales)
-        ws = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=q.device)
-        baps_attention_fwd_split(q, k, v, o, l, B, Hq, Hkv, Sq, Sk, D, causal, block, ws, nbytes, lam_, nb_,
-                                 scale_log2, restart_counts, stream, mode, restart_rows, b0_last, tile_counts,
-                                 qk_scales)
-    elif (lam is None and n_b0 is None and not scale_log2 and restart_counts is None and mode == BAPS_MODE_E2E_HIF8
-          and restart_rows == 1 and not b0_last and tile_counts is None and qk_scales is None):
-        baps_attention_fwd(q, k, v, o, l, B, Hq, Hkv, Sq, Sk, D, causal, block, stream)
-    else:
-        baps_attention_fwd_ex(q, k, v, o, l, B, Hq, Hkv, Sq, Sk, D, causal, block, lam_, nb_, scale_log2,
-                              restart_counts, stream, mode, restart_rows, b0_last, tile_counts, qk_scales)
-    return o, l
+    l = torch.empty((B, Hq, Sq), dtype=torch.float32, device=q.device)
+    baps_attention_fwd_dump(q, k, v, o, l, B, Hq, Hkv, Sq, Sk, D, causal, block, slot, acc, ref, stream,
+                            lam=lam, n_b0=n_b0, scale_log2=scale_log2, mode=mode, restart_rows=restart_rows,
+                            b0_last=b0_last, qk_scales=qk_scales, tie_mode=tie_mode, saturate=saturate)
+    return o, l, acc[:n, :Sk], ref[:n, :nblk]

@@ -22,6 +22,11 @@ __device__ __attribute__((aligned(256))) uint8_t g_code_table[kCodeTableBytes];
 // take the entry of kCodeLo, above kCodeHi that of kCodeHi), so that a lookup
 // needs no clamp; the prefill kernel copies it into LDS as it is.
 __device__ __attribute__((aligned(1024))) uint8_t g_code_table_x[kTabEntries];
+// Both tables for ties to even: the entry of an index is the P of the T whose
+// bits 31..19 are the index and whose bits 18..0 are zero (the one T of the
+// index that can be a tie); every other T reads the tables above.
+__device__ __attribute__((aligned(256))) uint8_t g_code_table_even[kCodeTableBytes];
+__device__ __attribute__((aligned(1024))) uint8_t g_code_table_x_even[kTabEntries];
 
 // HiF8 value of a double, rounded once: truncating to fp32 toward zero keeps
 // the sign, the exponent and the leading mantissa bits that decide a
@@ -62,8 +67,8 @@ uint8_t linear_code(float p)
 
 struct Table {
     uint32_t e[kTabEntries];
-    uint8_t code[kCodeEntries];
-    uint8_t codex[kTabEntries];
+    uint8_t code[kCodeEntries], code_even[kCodeEntries];
+    uint8_t codex[kTabEntries], codex_even[kTabEntries];
     Table()
     {
         for (uint32_t i = 0; i < (uint32_t)kTabEntries; ++i) {
@@ -72,8 +77,16 @@ struct Table {
             const uint32_t pb = hif8::f2u(p);
             e[i] = (pb & 0xffffff00u) | hif8::encode(p, true);
         }
-        for (int i = 0; i < kCodeEntries; ++i) code[i] = linear_code(hif8::u2f(e[kCodeLo + i] & 0xffffff00u));
-        for (int i = 0; i < kTabEntries; ++i) codex[i] = code[(i < kCodeLo ? kCodeLo : (i > kCodeHi ? kCodeHi : i)) - kCodeLo];
+        for (int i = 0; i < kCodeEntries; ++i) {
+            code[i] = linear_code(hif8::u2f(e[kCodeLo + i] & 0xffffff00u));
+            const float T = hif8::u2f((uint32_t)(kCodeLo + i) << kTabShift);
+            code_even[i] = linear_code(hif8_exp2(hif8::round(T, true, true)));
+        }
+        for (int i = 0; i < kTabEntries; ++i) {
+            const int ci = (i < kCodeLo ? kCodeLo : (i > kCodeHi ? kCodeHi : i)) - kCodeLo;
+            codex[i] = code[ci];
+            codex_even[i] = code_even[ci];
+        }
     }
 };
 
@@ -88,6 +101,8 @@ std::mutex g_mutex;
 const uint32_t* g_dev_table[kMaxDevices] = {};
 const uint8_t* g_dev_code[kMaxDevices] = {};
 const uint8_t* g_dev_codex[kMaxDevices] = {};
+const uint8_t* g_dev_code_even[kMaxDevices] = {};
+const uint8_t* g_dev_codex_even[kMaxDevices] = {};
 
 // the last HIP failure a call of this library met on the calling thread
 thread_local hipError_t g_last_hip = hipSuccess;
@@ -104,7 +119,25 @@ int status_of(hipError_t e)
 // their launches, so it is cleared first: a launch is judged on its own.
 void clear_stale_error() { (void)hipGetLastError(); }
 
-int table_on_current_device(const uint32_t** out, const uint8_t** code = nullptr, const uint8_t** codex = nullptr)
+// Upload one table to its device symbol; returns the symbol's device address.
+template <typename T, size_t N>
+int upload(const void* symbol, const T (&host)[N], const void** dev_addr)
+{
+    if (int st = status_of(hipMemcpyToSymbol(symbol, host, sizeof(host), 0, hipMemcpyHostToDevice))) return st;
+    void* ptr = nullptr;
+    if (int st = status_of(hipGetSymbolAddress(&ptr, symbol))) return st;
+    if (!ptr) return BAPS_HIP_ERROR;
+    *dev_addr = ptr;
+    return BAPS_OK;
+}
+
+struct DevTables {
+    const uint32_t* tab;
+    const uint8_t *code, *codex, *code_even, *codex_even;
+};
+
+int table_on_current_device(const uint32_t** out, const uint8_t** code = nullptr, const uint8_t** codex = nullptr,
+                            DevTables* all = nullptr)
 {
     int dev = 0;
     if (int st = status_of(hipGetDevice(&dev))) return st;
@@ -128,6 +161,11 @@ int table_on_current_device(const uint32_t** out, const uint8_t** code = nullptr
         void* xptr = nullptr;
         if (int st = status_of(hipGetSymbolAddress(&xptr, HIP_SYMBOL(g_code_table_x)))) return st;
         if (!ptr || !cptr || !xptr) return BAPS_HIP_ERROR;
+        const void *eptr = nullptr, *exptr = nullptr;
+        if (int st = upload(HIP_SYMBOL(g_code_table_even), t.code_even, &eptr)) return st;
+        if (int st = upload(HIP_SYMBOL(g_code_table_x_even), t.codex_even, &exptr)) return st;
+        g_dev_code_even[dev] = static_cast<const uint8_t*>(eptr);
+        g_dev_codex_even[dev] = static_cast<const uint8_t*>(exptr);
         g_dev_code[dev] = static_cast<const uint8_t*>(cptr);
         g_dev_codex[dev] = static_cast<const uint8_t*>(xptr);
         g_dev_table[dev] = static_cast<const uint32_t*>(ptr);
@@ -135,6 +173,8 @@ int table_on_current_device(const uint32_t** out, const uint8_t** code = nullptr
     *out = g_dev_table[dev];
     if (code) *code = g_dev_code[dev];
     if (codex) *codex = g_dev_codex[dev];
+    if (all) *all = DevTables{g_dev_table[dev], g_dev_code[dev], g_dev_codex[dev], g_dev_code_even[dev],
+                              g_dev_codex_even[dev]};
     return BAPS_OK;
 }
 
@@ -150,6 +190,7 @@ baps_params_t knobs_of(const baps_params_t* prm)
     k.lambda = 1;
     k.n_b0 = 1;
     k.mode = BAPS_MODE_E2E_HIF8;
+    k.saturate = 1;
     return k;
 }
 
@@ -199,6 +240,14 @@ int make_params(const void* q, const void* k, const void* v, float* o, float* ls
     const int R = effective_rows(kn.restart_rows, Sq);
     if (R > 1 && (mode != BAPS_MODE_E2E_HIF8 || !pow2(G) || G > 32 || (long long)R * G > 256 || f8))
         return BAPS_UNSUPPORTED;
+    if (kn.tie_mode != BAPS_TIES_AWAY && kn.tie_mode != BAPS_TIES_EVEN) return BAPS_INVALID_ARGUMENT;
+    const bool even = kn.tie_mode == BAPS_TIES_EVEN;
+    if (even && (mode != BAPS_MODE_E2E_HIF8 || kn.lambda > kCodeMaxLambda || R > 1 || f8)) return BAPS_UNSUPPORTED;
+    // without saturation a cast overflows only when an 8-bit P can exceed
+    // 2^15, i.e. from lambda 16 up (T <= lambda otherwise, and the eq. (2)
+    // setups have T <= 0): below that both settings give the same result
+    if (!kn.saturate && mode == BAPS_MODE_E2E_HIF8 && kn.lambda > 15) return BAPS_UNSUPPORTED;
+    if (kn.out_bf16 && !aligned16(o)) return BAPS_INVALID_ARGUMENT;
     AttnParams& p = *out;
     p.tab = nullptr;
     p.ctab = nullptr;
@@ -218,6 +267,14 @@ int make_params(const void* q, const void* k, const void* v, float* o, float* ls
     p.restart_rows = R;
     p.b0_last = kn.b0_last ? 1 : 0;
     p.qk_f8 = f8 ? 1 : 0;
+    p.out_bf16 = kn.out_bf16 ? 1 : 0;
+    p.tie_even = even ? 1 : 0;
+    p.ctab_even = nullptr;
+    p.ctabx_even = nullptr;
+    p.dump_slot = nullptr;
+    p.dump_acc = nullptr;
+    p.dump_ref = nullptr;
+    p.dump_nblk = 0;
     // the score scale in log2 units; with FP8 Q/K the dequantisation scales
     // fold into it, in double, rounded once
     const double base = kn.scale_log2 > 0.0f ? (double)kn.scale_log2 : 1.4426950408889634 / std::sqrt((double)D);
@@ -229,12 +286,13 @@ int make_params(const void* q, const void* k, const void* v, float* o, float* ls
 int attach_tables(AttnParams* p)
 {
     const uint32_t* tab = nullptr;
-    const uint8_t* ctab = nullptr;
-    const uint8_t* ctabx = nullptr;
-    const int st = table_on_current_device(&tab, &ctab, &ctabx);
-    p->tab = tab;
-    p->ctab = ctab;
-    p->ctabx = ctabx;
+    DevTables t{};
+    const int st = table_on_current_device(&tab, nullptr, nullptr, &t);
+    p->tab = t.tab;
+    p->ctab = t.code;
+    p->ctabx = t.codex;
+    p->ctab_even = t.code_even;
+    p->ctabx_even = t.codex_even;
     return st;
 }
 
@@ -266,7 +324,7 @@ SplitPlan split_plan(int B, int Hq, int Hkv, int Sq, int Sk, int D, int block, c
     SplitPlan sp;
     if (B <= 0 || Hq <= 0 || Hkv <= 0 || Sq <= 0 || Sk <= 0 || Hq % Hkv) return sp;
     if (!(D == 64 || D == 128) || !(block == 32 || block == 64 || block == 128)) return sp;
-    if (kn.mode != BAPS_MODE_E2E_HIF8 || kn.lambda > kCodeMaxLambda) return sp;
+    if (kn.mode != BAPS_MODE_E2E_HIF8 || kn.lambda > kCodeMaxLambda || kn.tie_mode != BAPS_TIES_AWAY) return sp;
     if (kn.restart_rows < 0 || effective_rows(kn.restart_rows, Sq) > 1) return sp;   // per-row decisions only
     const long long flat = (long long)Sq * (Hq / Hkv);
     if (flat > 64) return sp;                                   // the prefill kernel's regime
@@ -355,14 +413,37 @@ int baps_attention_fwd_ex(const void* q, const void* k, const void* v, float* o,
     }
 }
 
+int baps_attention_fwd_dump(const void* q, const void* k, const void* v, float* o, float* lse, int B, int Hq,
+                            int Hkv, int Sq, int Sk, int D, int causal, int block, const baps_params_t* prm,
+                            const int* row_slot, float* acc_out, float* ref_out, void* stream)
+{
+    try {
+        const baps_params_t kn = knobs_of(prm);
+        AttnParams p;
+        bool empty = false;
+        int st = make_params(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, kn, &p, &empty);
+        if (st || empty) return st;
+        if (!row_slot || (Sk > 0 && (!acc_out || !ref_out))) return BAPS_INVALID_ARGUMENT;
+        if ((st = attach_tables(&p))) return st;
+        p.dump_slot = row_slot;
+        p.dump_acc = acc_out;
+        p.dump_ref = ref_out;
+        p.dump_nblk = (Sk + block - 1) / block;
+        clear_stale_error();
+        return status_of(launch_attention(p, D, block, static_cast<hipStream_t>(stream)));
+    } catch (...) {
+        return BAPS_HIP_ERROR;
+    }
+}
+
 int hif8_encode(const float* x, unsigned char* codes, long long n, int flags, void* stream)
 {
-    if (n < 0 || (flags & ~BAPS_HIF8_SATURATE)) return BAPS_INVALID_ARGUMENT;
+    if (n < 0 || (flags & ~(BAPS_HIF8_SATURATE | BAPS_HIF8_TIES_EVEN))) return BAPS_INVALID_ARGUMENT;
     if (n == 0) return BAPS_OK;
     if (!x || !codes) return BAPS_INVALID_ARGUMENT;
     clear_stale_error();
     return status_of(launch_hif8_encode(x, codes, n, (flags & BAPS_HIF8_SATURATE) != 0,
-                                        static_cast<hipStream_t>(stream)));
+                                        (flags & BAPS_HIF8_TIES_EVEN) != 0, static_cast<hipStream_t>(stream)));
 }
 
 int hif8_decode(const unsigned char* codes, float* x, long long n, void* stream)

@@ -83,10 +83,14 @@ __device__ __forceinline__ void wait_vm(int n)
     }
 }
 
-template <int D, int BLK, bool CT, int MODE, bool F8>
+// TIE: the 8-bit cast of T rounds ties to even (a second code table covers
+// the T whose bits 18..0 are zero).  DUMP: also write the raw dot products and
+// block references of the rows the caller marks (AttnParams::dump_slot).
+template <int D, int BLK, bool CT, int MODE, bool F8, bool TIE, bool DUMP>
 __global__ __launch_bounds__(64 * (BLK / 32)) void baps_attn_decode_kernel(AttnParams p)
 {
     static_assert(MODE == kModeE2E || CT, "the eq. (2) setups use the compact table (T <= 0)");
+    static_assert(!TIE || (MODE == kModeE2E && CT && !F8), "ties to even: canonical path");
     static_assert(D == 64 || D == 128, "head dimension");
     static_assert(BLK % kSlotKeys == 0 && BLK <= 128, "key block");
     using C = DCfg<D, BLK>;
@@ -95,6 +99,7 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void baps_attn_decode_kernel(AttnP
     // P lookup: the compact code table (lambda <= kCodeMaxLambda), else the
     // bf16 half of the full score table
     __shared__ __attribute__((aligned(16))) uint8_t ctab[CT ? kCodeHi + 1 : 1];
+    __shared__ __attribute__((aligned(16))) uint8_t ctab_e[TIE ? kCodeHi + 1 : 1];
     __shared__ __attribute__((aligned(16))) uint16_t tab[CT ? 1 : kTabEntries];
     __shared__ float xch[2][KW][kRows];           // partial row maxima, by block parity
     extern __shared__ __attribute__((aligned(1024))) char ring[];
@@ -160,6 +165,8 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void baps_attn_decode_kernel(AttnP
         // fp32 exp2: no table
     } else if constexpr (CT) {
         for (int i = tid; i < kCodeEntries; i += 64 * KW) ctab[kCodeLo + i] = p.ctab[i];
+        if constexpr (TIE)
+            for (int i = tid; i < kCodeEntries; i += 64 * KW) ctab_e[kCodeLo + i] = p.ctab_even[i];
     } else {
         for (int i = tid; i < kTabEntries; i += 64 * KW) tab[i] = (uint16_t)(p.tab[i] >> 16);
     }
@@ -170,6 +177,8 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void baps_attn_decode_kernel(AttnP
     const int r = row_ok ? f / G : 0;
     const int h = g * G + (row_ok ? f % G : 0);
     const int kmax = row_ok ? (p.causal ? min(p.Sk - 1, r + off) : p.Sk - 1) : -1;
+    int dslot = -1;
+    if constexpr (DUMP) dslot = row_ok ? p.dump_slot[((long long)b * p.Hq + h) * p.Sq + r] : -1;
     // tile-level restart (restart_rows > 1, then restart_rows * G <= 16): the
     // rows c16 == h_local (mod G) of an aligned span of restart_rows * G rows
     // of the 16 share each block's decision; a ballot takes it
@@ -285,6 +294,18 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void baps_attn_decode_kernel(AttnP
                 for (int i = 0; i < 4; ++i)
                     if (16 * t2 + i > lim) sacc[t2][i] = ninf;
         }
+        if constexpr (DUMP) {
+            if (dslot >= 0) {
+                float* dst = p.dump_acc + (long long)dslot * p.Sk;
+#pragma unroll
+                for (int t2 = 0; t2 < 2; ++t2)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int key = key0 + 16 * t2 + 4 * grp + i;
+                        if (key <= kmax) dst[key] = sacc[t2][i];
+                    }
+            }
+        }
         // row maximum of the block: this wave's 32 keys, then across the waves
         float pm = __builtin_fmaxf(__builtin_fmaxf(__builtin_fmaxf(sacc[0][0], sacc[0][1]), sacc[0][2]),
                                    __builtin_fmaxf(__builtin_fmaxf(sacc[0][3], sacc[1][0]), sacc[1][1]));
@@ -307,7 +328,7 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void baps_attn_decode_kernel(AttnP
             const bool vis = row_ok && amax != ninf;
             const bool in_b0 = (jb < p.n_b0) || (p.b0_last && jb == kmax / BLK);
             const bool forced = in_b0 || (m == ninf);
-            const float tq = hif8::round(__builtin_fmaf(amax, c, -m));
+            const float tq = hif8::round(__builtin_fmaf(amax, c, -m), true, TIE);
             bool restart = forced || (ceilf(tq) > lam);
             bool b1 = vis && !in_b0;
             if (tiled) {
@@ -333,6 +354,9 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void baps_attn_decode_kernel(AttnP
             m = m_new;
             ref = ref_new;
             nref = (ref == ninf) ? 0.0f : -ref;
+            if constexpr (DUMP) {
+                if (dslot >= 0 && grp == 0 && wave == 0 && vis) p.dump_ref[(long long)dslot * p.dump_nblk + jb] = ref;
+            }
         } else {
             // eq. (2): real-valued running maximum (see the prefill kernel)
             const bool vis = amax != ninf;
@@ -357,6 +381,9 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void baps_attn_decode_kernel(AttnP
             m = m_new;
             ref = m_new;
             nref = (m == ninf) ? 0.0f : -m;
+            if constexpr (DUMP) {
+                if (dslot >= 0 && grp == 0 && wave == 0 && vis) p.dump_ref[(long long)dslot * p.dump_nblk + jb] = ref;
+            }
         }
 
         // P = HiF8(2^HiF8(T)) of the 32 keys as one B operand: slots 0..3 =
@@ -378,7 +405,15 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void baps_attn_decode_kernel(AttnP
                                               : sacc[t2][2 * (e & 1)] * c + nref;
             const float t1 = MODE == kModeE2E ? __builtin_fmaf(sacc[t2][2 * (e & 1) + 1], c, nref)
                                               : sacc[t2][2 * (e & 1) + 1] * c + nref;
-            if constexpr (CT) {
+            if constexpr (TIE) {
+                // a T with bits 18..0 zero reads the ties-to-even table
+                const uint32_t u0 = hif8::f2u(t0), u1 = hif8::f2u(t1);
+                const uint32_t i0 = min(max(u0 >> kTabShift, (uint32_t)kCodeLo), (uint32_t)kCodeHi);
+                const uint32_t i1 = min(max(u1 >> kTabShift, (uint32_t)kCodeLo), (uint32_t)kCodeHi);
+                const uint32_t c0 = (u0 & 0x7ffffu) ? ctab[i0] : ctab_e[i0];
+                const uint32_t c1 = (u1 & 0x7ffffu) ? ctab[i1] : ctab_e[i1];
+                w = (c0 | (c1 << 16)) << 4;
+            } else if constexpr (CT) {
                 const uint32_t i0 = min(max(hif8::f2u(t0) >> kTabShift, (uint32_t)kCodeLo), (uint32_t)kCodeHi);
                 const uint32_t i1 = min(max(hif8::f2u(t1) >> kTabShift, (uint32_t)kCodeLo), (uint32_t)kCodeHi);
                 w = ((uint32_t)ctab[i0] | ((uint32_t)ctab[i1] << 16)) << 4;
@@ -435,15 +470,27 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void baps_attn_decode_kernel(AttnP
         }
     }
     if (!row_ok) return;
-    float* orow = p.o + (((long long)b * p.Hq + h) * p.Sq + r) * D;
+    const long long orow_off = (((long long)b * p.Hq + h) * p.Sq + r) * D;
     const bool empty = (ref == ninf);
     const float inv = empty ? 0.0f : 1.0f / dw;
+    if (p.out_bf16) {
+        uint16_t* orow = reinterpret_cast<uint16_t*>(p.o) + orow_off;
 #pragma unroll
-    for (int t = 0; t < kDT; ++t) {
-        f32x4 v;
+        for (int t = 0; t < kDT; ++t) {
+            const bf16x2 lo = {(__bf16)(oacc[t][0] * inv), (__bf16)(oacc[t][1] * inv)};
+            const bf16x2 hi = {(__bf16)(oacc[t][2] * inv), (__bf16)(oacc[t][3] * inv)};
+            *reinterpret_cast<u32x2*>(orow + 16 * t + 4 * grp) =
+                u32x2{__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
+        }
+    } else {
+        float* orow = p.o + orow_off;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = oacc[t][e] * inv;
-        *reinterpret_cast<f32x4*>(orow + 16 * t + 4 * grp) = v;
+        for (int t = 0; t < kDT; ++t) {
+            f32x4 v;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = oacc[t][e] * inv;
+            *reinterpret_cast<f32x4*>(orow + 16 * t + 4 * grp) = v;
+        }
     }
     if (grp == 0) {
         const float dbias = (CT && MODE != kModeDefault) ? (float)kCodeBiasLog2 : 0.0f;
@@ -464,7 +511,7 @@ __global__ __launch_bounds__(64 * (BLK / 32)) void baps_attn_decode_kernel(AttnP
     }
 }
 
-template <int D, int BLK, bool CT, int MODE, bool F8 = false>
+template <int D, int BLK, bool CT, int MODE, bool F8, bool TIE, bool DUMP>
 hipError_t launch_dec(const AttnParams& p, hipStream_t st)
 {
     using C = DCfg<D, BLK>;
@@ -474,42 +521,50 @@ hipError_t launch_dec(const AttnParams& p, hipStream_t st)
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
     if (!attr_set.is_done(dev)) {
-        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&baps_attn_decode_kernel<D, BLK, CT, MODE, F8>),
+        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&baps_attn_decode_kernel<D, BLK, CT, MODE, F8, TIE, DUMP>),
                                 hipFuncAttributeMaxDynamicSharedMemorySize, C::kLdsBytes);
         if (e != hipSuccess) return e;
         attr_set.mark(dev);
     }
     const long long flat = (long long)p.Sq * (p.Hq / p.Hkv);
     const dim3 grid((unsigned)((flat + kRows - 1) / kRows), (unsigned)p.Hkv, (unsigned)p.B);
-    hipLaunchKernelGGL((baps_attn_decode_kernel<D, BLK, CT, MODE, F8>), grid, dim3(64 * C::kWaves), C::kLdsBytes, st, p);
+    hipLaunchKernelGGL((baps_attn_decode_kernel<D, BLK, CT, MODE, F8, TIE, DUMP>), grid, dim3(64 * C::kWaves),
+                       C::kLdsBytes, st, p);
     return hipGetLastError();
 }
 
-template <int D, int BLK>
+template <int D, int BLK, bool DUMP>
 hipError_t launch_dec_ct(const AttnParams& p, hipStream_t st)
 {
+    if (p.tie_even) return launch_dec<D, BLK, true, kModeE2E, false, true, DUMP>(p, st);
     if (p.qk_f8) {                                 // FP8 Q/K
-        if (p.mode == kModeDefault) return launch_dec<D, BLK, true, kModeDefault, true>(p, st);
-        if (p.mode == kModeExp2) return launch_dec<D, BLK, true, kModeExp2, true>(p, st);
-        if (p.lambda <= kCodeMaxLambda) return launch_dec<D, BLK, true, kModeE2E, true>(p, st);
-        return launch_dec<D, BLK, false, kModeE2E, true>(p, st);
+        if (p.mode == kModeDefault) return launch_dec<D, BLK, true, kModeDefault, true, false, DUMP>(p, st);
+        if (p.mode == kModeExp2) return launch_dec<D, BLK, true, kModeExp2, true, false, DUMP>(p, st);
+        if (p.lambda <= kCodeMaxLambda) return launch_dec<D, BLK, true, kModeE2E, true, false, DUMP>(p, st);
+        return launch_dec<D, BLK, false, kModeE2E, true, false, DUMP>(p, st);
     }
-    if (p.mode == kModeDefault) return launch_dec<D, BLK, true, kModeDefault>(p, st);
-    if (p.mode == kModeExp2) return launch_dec<D, BLK, true, kModeExp2>(p, st);
-    if (p.lambda <= kCodeMaxLambda) return launch_dec<D, BLK, true, kModeE2E>(p, st);
-    return launch_dec<D, BLK, false, kModeE2E>(p, st);
+    if (p.mode == kModeDefault) return launch_dec<D, BLK, true, kModeDefault, false, false, DUMP>(p, st);
+    if (p.mode == kModeExp2) return launch_dec<D, BLK, true, kModeExp2, false, false, DUMP>(p, st);
+    if (p.lambda <= kCodeMaxLambda) return launch_dec<D, BLK, true, kModeE2E, false, false, DUMP>(p, st);
+    return launch_dec<D, BLK, false, kModeE2E, false, false, DUMP>(p, st);
+}
+
+template <int D, int BLK>
+hipError_t launch_dec_any(const AttnParams& p, hipStream_t st)
+{
+    return p.dump_slot ? launch_dec_ct<D, BLK, true>(p, st) : launch_dec_ct<D, BLK, false>(p, st);
 }
 
 }  // namespace
 
 hipError_t launch_attention_decode(const AttnParams& p, int D, int block, hipStream_t st)
 {
-    if (D == 64 && block == 32) return launch_dec_ct<64, 32>(p, st);
-    if (D == 64 && block == 64) return launch_dec_ct<64, 64>(p, st);
-    if (D == 64 && block == 128) return launch_dec_ct<64, 128>(p, st);
-    if (D == 128 && block == 32) return launch_dec_ct<128, 32>(p, st);
-    if (D == 128 && block == 64) return launch_dec_ct<128, 64>(p, st);
-    if (D == 128 && block == 128) return launch_dec_ct<128, 128>(p, st);
+    if (D == 64 && block == 32) return launch_dec_any<64, 32>(p, st);
+    if (D == 64 && block == 64) return launch_dec_any<64, 64>(p, st);
+    if (D == 64 && block == 128) return launch_dec_any<64, 128>(p, st);
+    if (D == 128 && block == 32) return launch_dec_any<128, 32>(p, st);
+    if (D == 128 && block == 64) return launch_dec_any<128, 64>(p, st);
+    if (D == 128 && block == 128) return launch_dec_any<128, 128>(p, st);
     return hipErrorInvalidValue;
 }
 

@@ -292,19 +292,23 @@ __device__ __forceinline__ bool item_of_round(kargs_ptr a, int r, ItemGeo& e)
 
 // PERSIST: the grid holds at most as many workgroups as the GPU runs at once
 // and each takes a sequence of items (item_at); otherwise one item per
-// workgroup.
-template <int D, int BLK, int NW, bool CT, int MODE, bool TILE, bool F8, bool PERSIST>
+// workgroup.  TIE: the 8-bit cast of T rounds ties to even (a second code
+// table covers the T whose bits 18..0 are zero, the only ones that can sit
+// exactly halfway).  DUMP: also write the raw dot products and the block
+// references of the rows the caller marks (AttnParams::dump_slot).
+template <int D, int BLK, int NW, bool CT, int MODE, bool TILE, bool F8, bool PERSIST, bool TIE, bool DUMP>
 __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
 {
     static_assert(MODE == kModeE2E || CT, "the eq. (2) setups use the compact table (T <= 0)");
     static_assert(MODE == kModeE2E || !TILE, "tile-level restart belongs to Alg. 1");
+    static_assert(!TIE || (MODE == kModeE2E && CT && !TILE && !F8), "ties to even: canonical per-row path");
     static_assert(D == 64 || D == 128, "head dimension");
     static_assert(BLK % 32 == 0 && BLK <= 128, "key block");
     using C = Cfg<D, BLK, NW>;
     // P lookup: with the code table (lambda <= kCodeMaxLambda) the table
     // expanded to all 8192 indices (no lookup needs a clamp); else the bf16
     // half of the full score table
-    __shared__ __attribute__((aligned(1024))) uint8_t ctab[CT ? kTabEntries : 1];
+    __shared__ __attribute__((aligned(1024))) uint8_t ctab[CT ? (TIE ? 2 : 1) * kTabEntries : 1];
     __shared__ __attribute__((aligned(16))) uint16_t tab[CT ? 1 : kTabEntries];
     __shared__ uint32_t tflag[TILE ? NW : 1][3];  // per wave: rows that restart, see the block, are in B0
     extern __shared__ __attribute__((aligned(1024))) char tiles[];
@@ -449,6 +453,11 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
             const uint32_t ct_lds = (uint32_t)(uintptr_t)LDS_PTR(uint8_t, ctab);
             for (int i = wave; i < kTabEntries / 1024; i += NW)
                 lds_dma_16(p.ctabx + i * 1024 + 16 * lane, __builtin_amdgcn_readfirstlane(ct_lds + i * 1024));
+            if constexpr (TIE) {
+                for (int i = wave; i < kTabEntries / 1024; i += NW)
+                    lds_dma_16(p.ctabx_even + i * 1024 + 16 * lane,
+                               __builtin_amdgcn_readfirstlane(ct_lds + kTabEntries + i * 1024));
+            }
         } else {
             for (int i = tid; i < kTabEntries; i += C::kThreads) tab[i] = (uint16_t)(p.tab[i] >> 16);
         }
@@ -474,6 +483,8 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
         const int r = row_ok ? f / Gi : 0;
         const int h = cur.g * Gi + (row_ok ? f % Gi : 0);
         const int kmax = row_ok ? (p.causal ? min(p.Sk - 1, r + off) : p.Sk - 1) : -1;
+        int dslot = -1;
+        if constexpr (DUMP) dslot = row_ok ? p.dump_slot[((long long)cur.b * p.Hq + h) * p.Sq + r] : -1;
         int kmax_wave_hi = kmax, kmax_wave_lo = row_ok ? kmax : 0x7fffffff;
 #pragma unroll
         for (int o = 1; o < 64; o <<= 1) {
@@ -584,6 +595,18 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
                     for (int i = 0; i < 16; ++i)
                         if (kt * 32 + 8 * (i / 4) + (i % 4) > lim) sacc[kt][i] = ninf;
             }
+            if constexpr (DUMP) {
+                if (dslot >= 0) {
+                    float* dst = p.dump_acc + (long long)dslot * p.Sk;
+#pragma unroll
+                    for (int kt = 0; kt < kKT; ++kt)
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) {
+                            const int key = key0 + 32 * kt + 8 * (i / 4) + 4 * half + i % 4;
+                            if (key <= kmax) dst[key] = sacc[kt][i];
+                        }
+                }
+            }
             // row maximum of the raw dot products (the scale c > 0 is monotone):
             // a 3-way tree over this lane's 16*kKT scores, then lanes l and l^32
             {
@@ -606,7 +629,7 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
                 const bool vis = (!TILE || row_ok) && amax != ninf;
                 const bool in_b0 = (jb < p.n_b0) || (p.b0_last && jb == kmax / BLK);
                 const bool forced = in_b0 || (m == ninf);
-                const float tq = hif8::round(__builtin_fmaf(amax, c, -m));
+                const float tq = hif8::round(__builtin_fmaf(amax, c, -m), true, TIE);
                 bool restart = forced || (ceilf(tq) > lam);
                 if constexpr (TILE) {
                     // the tile restarts when any of its rows that see the block would
@@ -658,6 +681,9 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
                 dl *= f;
                 m = m_new;
                 ref = ref_new;
+                if constexpr (DUMP) {
+                    if (dslot >= 0 && half == 0 && vis) p.dump_ref[(long long)dslot * p.dump_nblk + jb] = ref;
+                }
     
                 // a row with no visible key so far keeps ref = -inf; its masked scores
                 // (acc = -inf) must still give T = -inf and P = 0
@@ -686,6 +712,9 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
                 m = m_new;
                 ref = m_new;
                 nref = (m == ninf) ? 0.0f : -m;
+                if constexpr (DUMP) {
+                    if (dslot >= 0 && half == 0 && vis) p.dump_ref[(long long)dslot * p.dump_nblk + jb] = ref;
+                }
             }
     
             if (!live) continue;
@@ -716,7 +745,13 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
                                                           : sacc[kt][ch * 8 + 2 * e] * c + nref;
                         const float t1 = MODE == kModeE2E ? __builtin_fmaf(sacc[kt][ch * 8 + 2 * e + 1], c, nref)
                                                           : sacc[kt][ch * 8 + 2 * e + 1] * c + nref;
-                        if constexpr (CT) {
+                        if constexpr (TIE) {
+                            // a T with bits 18..0 zero reads the ties-to-even half of the table
+                            const uint32_t u0 = hif8::f2u(t0), u1 = hif8::f2u(t1);
+                            const uint32_t i0 = (u0 >> kTabShift) | ((u0 & 0x7ffffu) ? 0u : (uint32_t)kTabEntries);
+                            const uint32_t i1 = (u1 >> kTabShift) | ((u1 & 0x7ffffu) ? 0u : (uint32_t)kTabEntries);
+                            w = ((uint32_t)ctab[i0] | ((uint32_t)ctab[i1] << 16)) << 4;
+                        } else if constexpr (CT) {
                             // two bf16 of P * 2^-kCodeBiasLog2
                             w = ((uint32_t)ctab[hif8::f2u(t0) >> kTabShift] | ((uint32_t)ctab[hif8::f2u(t1) >> kTabShift] << 16)) << 4;
                         } else {
@@ -749,18 +784,32 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
         const float dbias = (CT && MODE != kModeDefault) ? (float)kCodeBiasLog2 : 0.0f;
         const kargs_ptr a = fresh_args();
         if (row_ok) {
-            float* orow = a->o + (((long long)cur.b * a->Hq + h) * a->Sq + r) * D;
+            const long long orow_off = (((long long)cur.b * a->Hq + h) * a->Sq + r) * D;
             const bool empty = (ref == ninf);
             const float inv = empty ? 0.0f : 1.0f / d;
+            if (a->out_bf16) {
+                uint16_t* orow = reinterpret_cast<uint16_t*>(a->o) + orow_off;
 #pragma unroll
-            for (int t = 0; t < kDT; ++t)
+                for (int t = 0; t < kDT; ++t)
 #pragma unroll
-                for (int q4 = 0; q4 < 4; ++q4) {
-                    f32x4 v;
+                    for (int q4 = 0; q4 < 4; ++q4) {
+                        const bf16x2 lo = {(__bf16)(oacc[t][q4 * 4 + 0] * inv), (__bf16)(oacc[t][q4 * 4 + 1] * inv)};
+                        const bf16x2 hi = {(__bf16)(oacc[t][q4 * 4 + 2] * inv), (__bf16)(oacc[t][q4 * 4 + 3] * inv)};
+                        *reinterpret_cast<u32x2*>(orow + t * 32 + q4 * 8 + half * 4) =
+                            u32x2{__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
+                    }
+            } else {
+                float* orow = a->o + orow_off;
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) v[e] = oacc[t][q4 * 4 + e] * inv;
-                    *reinterpret_cast<f32x4*>(orow + t * 32 + q4 * 8 + half * 4) = v;
-                }
+                for (int t = 0; t < kDT; ++t)
+#pragma unroll
+                    for (int q4 = 0; q4 < 4; ++q4) {
+                        f32x4 v;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) v[e] = oacc[t][q4 * 4 + e] * inv;
+                        *reinterpret_cast<f32x4*>(orow + t * 32 + q4 * 8 + half * 4) = v;
+                    }
+            }
             if (half == 0) {
                 if (a->lse)
                     a->lse[((long long)cur.b * a->Hq + h) * a->Sq + r] =
@@ -791,7 +840,7 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
     }
 }
 
-template <int D, int BLK, int NW, bool CT, int MODE, bool TILE = false, bool F8 = false>
+template <int D, int BLK, int NW, bool CT, int MODE, bool TILE, bool F8, bool TIE, bool DUMP>
 hipError_t launch_one(const AttnParams& p, hipStream_t st)
 {
     using C = Cfg<D, BLK, NW>;
@@ -801,7 +850,8 @@ hipError_t launch_one(const AttnParams& p, hipStream_t st)
     // whose extra state would spill across the item loop
     constexpr bool kPersist = D == 128 && !TILE;
     const int lds = 4 * C::kTileBytes;
-    const void* fn = reinterpret_cast<const void*>(&baps_attn_fwd_kernel<D, BLK, NW, CT, MODE, TILE, F8, kPersist>);
+    const void* fn =
+        reinterpret_cast<const void*>(&baps_attn_fwd_kernel<D, BLK, NW, CT, MODE, TILE, F8, kPersist, TIE, DUMP>);
     int dev = 0, ncu = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e == hipSuccess) e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
@@ -825,13 +875,13 @@ hipError_t launch_one(const AttnParams& p, hipStream_t st)
     const long long items = (flat + C::kTileRows - 1) / C::kTileRows * p.Hkv * p.B;
     const long long slots = (long long)ncu * per_cu;
     const unsigned grid = (unsigned)(kPersist && items > slots ? slots : items);
-    hipLaunchKernelGGL((baps_attn_fwd_kernel<D, BLK, NW, CT, MODE, TILE, F8, kPersist>), dim3(grid), dim3(C::kThreads),
-                       lds, st, p);
+    hipLaunchKernelGGL((baps_attn_fwd_kernel<D, BLK, NW, CT, MODE, TILE, F8, kPersist, TIE, DUMP>), dim3(grid),
+                       dim3(C::kThreads), lds, st, p);
     return hipGetLastError();
 }
 
-template <int D, int BLK>
-hipError_t launch_d_blk(const AttnParams& p, hipStream_t st)
+template <int D, int BLK, bool DUMP>
+hipError_t launch_d_blk_dump(const AttnParams& p, hipStream_t st)
 {
     // few rows per key/value head (decode, short queries): the HBM-streaming
     // kernel, which holds a tile of restart_rows query positions when it fits
@@ -839,20 +889,28 @@ hipError_t launch_d_blk(const AttnParams& p, hipStream_t st)
     const int G = p.Hq / p.Hkv;
     const long long flat = (long long)p.Sq * G;
     if (flat <= 64 && (long long)p.restart_rows * G <= 16) return launch_attention_decode(p, D, BLK, st);
+    if (p.tie_even)                                // ties to even (canonical per-row path only)
+        return launch_one<D, BLK, 8, true, kModeE2E, false, false, true, DUMP>(p, st);
     if (p.qk_f8) {                                 // FP8 Q/K (per-row restart only)
-        if (p.mode == kModeDefault) return launch_one<D, BLK, 8, true, kModeDefault, false, true>(p, st);
-        if (p.mode == kModeExp2) return launch_one<D, BLK, 8, true, kModeExp2, false, true>(p, st);
-        if (p.lambda <= kCodeMaxLambda) return launch_one<D, BLK, 8, true, kModeE2E, false, true>(p, st);
-        return launch_one<D, BLK, 8, false, kModeE2E, false, true>(p, st);
+        if (p.mode == kModeDefault) return launch_one<D, BLK, 8, true, kModeDefault, false, true, false, DUMP>(p, st);
+        if (p.mode == kModeExp2) return launch_one<D, BLK, 8, true, kModeExp2, false, true, false, DUMP>(p, st);
+        if (p.lambda <= kCodeMaxLambda) return launch_one<D, BLK, 8, true, kModeE2E, false, true, false, DUMP>(p, st);
+        return launch_one<D, BLK, 8, false, kModeE2E, false, true, false, DUMP>(p, st);
     }
-    if (p.mode == kModeDefault) return launch_one<D, BLK, 8, true, kModeDefault>(p, st);
-    if (p.mode == kModeExp2) return launch_one<D, BLK, 8, true, kModeExp2>(p, st);
+    if (p.mode == kModeDefault) return launch_one<D, BLK, 8, true, kModeDefault, false, false, false, DUMP>(p, st);
+    if (p.mode == kModeExp2) return launch_one<D, BLK, 8, true, kModeExp2, false, false, false, DUMP>(p, st);
     if (p.restart_rows > 1) {
-        if (p.lambda <= kCodeMaxLambda) return launch_one<D, BLK, 8, true, kModeE2E, true>(p, st);
-        return launch_one<D, BLK, 8, false, kModeE2E, true>(p, st);
+        if (p.lambda <= kCodeMaxLambda) return launch_one<D, BLK, 8, true, kModeE2E, true, false, false, DUMP>(p, st);
+        return launch_one<D, BLK, 8, false, kModeE2E, true, false, false, DUMP>(p, st);
     }
-    if (p.lambda <= kCodeMaxLambda) return launch_one<D, BLK, 8, true, kModeE2E>(p, st);
-    return launch_one<D, BLK, 8, false, kModeE2E>(p, st);
+    if (p.lambda <= kCodeMaxLambda) return launch_one<D, BLK, 8, true, kModeE2E, false, false, false, DUMP>(p, st);
+    return launch_one<D, BLK, 8, false, kModeE2E, false, false, false, DUMP>(p, st);
+}
+
+template <int D, int BLK>
+hipError_t launch_d_blk(const AttnParams& p, hipStream_t st)
+{
+    return p.dump_slot ? launch_d_blk_dump<D, BLK, true>(p, st) : launch_d_blk_dump<D, BLK, false>(p, st);
 }
 
 }  // namespace

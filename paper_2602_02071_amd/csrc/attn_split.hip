@@ -629,8 +629,16 @@ __global__ __launch_bounds__(256) void split_combine_kernel(SplitParams sp)
     const int h = g * G + f % G;
     const bool empty = rr == ninf;
     const float inv = empty ? 0.0f : 1.0f / dx;
-    float* orow = p.o + (((long long)b * p.Hq + h) * p.Sq + r) * D + 4 * q4;
-    *reinterpret_cast<f32x4*>(orow) = f32x4{xs[0] * inv, xs[1] * inv, xs[2] * inv, xs[3] * inv};
+    const long long orow_off = (((long long)b * p.Hq + h) * p.Sq + r) * D + 4 * q4;
+    if (p.out_bf16) {
+        typedef __bf16 bf16x2 __attribute__((__vector_size__(2 * sizeof(__bf16))));
+        const bf16x2 lo = {(__bf16)(xs[0] * inv), (__bf16)(xs[1] * inv)};
+        const bf16x2 hi = {(__bf16)(xs[2] * inv), (__bf16)(xs[3] * inv)};
+        *reinterpret_cast<u32x2*>(reinterpret_cast<uint16_t*>(p.o) + orow_off) =
+            u32x2{__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
+    } else {
+        *reinterpret_cast<f32x4*>(p.o + orow_off) = f32x4{xs[0] * inv, xs[1] * inv, xs[2] * inv, xs[3] * inv};
+    }
     if (q4 == 0 && p.lse)
         p.lse[((long long)b * p.Hq + h) * p.Sq + r] =
             empty ? ninf : 0.69314718055994531f * (rr + (log2f(dx) + (float)kCodeBiasLog2));

@@ -18,28 +18,39 @@ constexpr int kUnroll = 4;                     // 4-element groups per lane per 
 // so each workgroup tabulates the code of every such prefix once (8 KiB of
 // LDS) and the streaming loop is a shift and a table read.  The one case the
 // prefix cannot tell is a NaN whose payload sits below bit 19: its prefix
-// reads as +-Inf, so NaN is tested on the full pattern.
+// reads as +-Inf, so NaN is tested on the full pattern.  With ties to even
+// (EVEN) an input can sit exactly halfway only when bits 18..0 are zero: a
+// second table holds the code of each prefix with those bits zero, and every
+// other input is not a tie, where both rules agree.
+template <bool EVEN>
 __device__ __forceinline__ uint32_t encode1(const uint8_t* tab8, float x)
 {
     const uint32_t u = hif8::f2u(x);
-    const uint32_t c = tab8[u >> kTabShift];
+    uint32_t i = u >> kTabShift;
+    if constexpr (EVEN) i |= (u & 0x7ffffu) ? 0u : (uint32_t)kTabEntries;
+    const uint32_t c = tab8[i];
     return (u & 0x7fffffffu) > 0x7f800000u ? 0x80u : c;
 }
 
+template <bool EVEN>
 __device__ __forceinline__ uint32_t encode4(const uint8_t* tab8, f32x4 v)
 {
-    return encode1(tab8, v[0]) | (encode1(tab8, v[1]) << 8) | (encode1(tab8, v[2]) << 16) |
-           (encode1(tab8, v[3]) << 24);
+    return encode1<EVEN>(tab8, v[0]) | (encode1<EVEN>(tab8, v[1]) << 8) | (encode1<EVEN>(tab8, v[2]) << 16) |
+           (encode1<EVEN>(tab8, v[3]) << 24);
 }
 
+template <bool EVEN>
 __global__ __launch_bounds__(kThreads) void hif8_encode_kernel(const float* __restrict__ x,
                                                                uint8_t* __restrict__ codes,
                                                                long long n, int saturate)
 {
     const bool sat = saturate != 0;
-    __shared__ uint8_t tab8[kTabEntries];
-    for (int i = threadIdx.x; i < kTabEntries; i += kThreads)
-        tab8[i] = hif8::encode(hif8::u2f((uint32_t)i << kTabShift), sat);
+    __shared__ uint8_t tab8[(EVEN ? 2 : 1) * kTabEntries];
+    for (int i = threadIdx.x; i < kTabEntries; i += kThreads) {
+        const float xi = hif8::u2f((uint32_t)i << kTabShift);
+        tab8[i] = hif8::encode(xi, sat);
+        if constexpr (EVEN) tab8[kTabEntries + i] = hif8::encode(xi, sat, true);
+    }
     __syncthreads();
     const long long ngroups = n / 4;                              // 4-element groups
     const long long per_iter = (long long)gridDim.x * kThreads * kUnroll;
@@ -55,21 +66,21 @@ __global__ __launch_bounds__(kThreads) void hif8_encode_kernel(const float* __re
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
             const long long gi = g0 + (long long)u * kThreads;
-            if (gi < ngroups) __builtin_nontemporal_store(encode4(tab8, v[u]), dst + gi);
+            if (gi < ngroups) __builtin_nontemporal_store(encode4<EVEN>(tab8, v[u]), dst + gi);
         }
     }
     // ragged tail (fewer than 4 elements)
     const long long i = ngroups * 4 + (long long)blockIdx.x * kThreads + threadIdx.x;
-    if (blockIdx.x == 0 && i < n) codes[i] = (uint8_t)encode1(tab8, x[i]);
+    if (blockIdx.x == 0 && i < n) codes[i] = (uint8_t)encode1<EVEN>(tab8, x[i]);
 }
 
 __global__ __launch_bounds__(kThreads) void hif8_encode_scalar_kernel(const float* __restrict__ x,
                                                                       uint8_t* __restrict__ codes,
-                                                                      long long n, int saturate)
+                                                                      long long n, int saturate, int even)
 {
     const long long stride = (long long)gridDim.x * kThreads;
     for (long long i = (long long)blockIdx.x * kThreads + threadIdx.x; i < n; i += stride)
-        codes[i] = hif8::encode(x[i], saturate != 0);
+        codes[i] = hif8::encode(x[i], saturate != 0, even != 0);
 }
 
 __global__ __launch_bounds__(kThreads) void hif8_decode_kernel(const uint8_t* __restrict__ codes,
@@ -121,15 +132,17 @@ int grid_for(long long work_items)
 
 }  // namespace
 
-hipError_t launch_hif8_encode(const float* x, uint8_t* codes, long long n, bool saturate, hipStream_t st)
+hipError_t launch_hif8_encode(const float* x, uint8_t* codes, long long n, bool saturate, bool even, hipStream_t st)
 {
     const bool aligned = ((uintptr_t)x % 16 == 0) && ((uintptr_t)codes % 4 == 0);
-    if (aligned)
-        hipLaunchKernelGGL(hif8_encode_kernel, dim3(grid_for(n / (4 * kUnroll) + 1)), dim3(kThreads), 0, st,
-                           x, codes, n, (int)saturate);
+    const dim3 grid(grid_for(n / (4 * kUnroll) + 1));
+    if (aligned && even)
+        hipLaunchKernelGGL(hif8_encode_kernel<true>, grid, dim3(kThreads), 0, st, x, codes, n, (int)saturate);
+    else if (aligned)
+        hipLaunchKernelGGL(hif8_encode_kernel<false>, grid, dim3(kThreads), 0, st, x, codes, n, (int)saturate);
     else
         hipLaunchKernelGGL(hif8_encode_scalar_kernel, dim3(grid_for(n)), dim3(kThreads), 0, st,
-                           x, codes, n, (int)saturate);
+                           x, codes, n, (int)saturate, (int)even);
     return hipGetLastError();
 }
 

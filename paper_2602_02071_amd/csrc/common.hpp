@@ -84,6 +84,19 @@ struct AttnParams {
     int b0_last;                // B0 also holds each row's last visible key block
     int qk_f8;                  // q and k hold FP8 E4M3 codes (c already holds the scales)
     float c;                    // log2(e)/sqrt(D) as fp32 (or the caller's override)
+    int out_bf16;               // o holds bf16 (round to nearest even of the fp32 result)
+    int tie_even;               // the 8-bit cast of T rounds ties to even (kernels built with TIE)
+    const uint8_t* ctab_even;   // compact code table for exact ties under ties-to-even (device)
+    const uint8_t* ctabx_even;  // the same expanded to all kTabEntries indices (device)
+    // Score dump (kernels built with DUMP only): a query row whose
+    // dump_slot[(b*Hq + h)*Sq + r] is s >= 0 writes its raw dot products q.k
+    // to dump_acc[s*Sk + key] for every key it sees, and its reference (Alg.
+    // 1's m~; the running maximum in the eq. (2) setups) after every key block
+    // j it sees to dump_ref[s*dump_nblk + j]
+    const int* dump_slot;
+    float* dump_acc;
+    float* dump_ref;
+    int dump_nblk;
 };
 
 struct SoftmaxBlockParams {
@@ -165,7 +178,7 @@ __device__ __forceinline__ float wave_sum(float v)
 }
 
 // Host launchers (one per kernel family); return a hipError_t.
-hipError_t launch_hif8_encode(const float* x, uint8_t* codes, long long n, bool saturate, hipStream_t st);
+hipError_t launch_hif8_encode(const float* x, uint8_t* codes, long long n, bool saturate, bool even, hipStream_t st);
 hipError_t launch_hif8_decode(const uint8_t* codes, float* x, long long n, hipStream_t st);
 hipError_t launch_softmax_block(const SoftmaxBlockParams& p, hipStream_t st);
 hipError_t launch_attention(const AttnParams& p, int D, int block, hipStream_t st);

@@ -7,10 +7,12 @@
 // 1 bit for +-8..+-15, and powers of two only (denormals) from 2^-22 to
 // 2^-16.  The largest finite value is 2^15.
 //
-// Rounding is to nearest with ties away from zero, straight from the fp32
-// input (one rounding).  For ties-away rounding only the first dropped
-// mantissa bit matters, so the rounded value of x depends on nothing but
-// the sign, the exponent and the top four mantissa bits of x: bits 31..19.
+// Rounding is to nearest with ties away from zero (or, on request, to even),
+// straight from the fp32 input (one rounding).  For ties-away rounding only
+// the first dropped mantissa bit matters, so the rounded value of x depends
+// on nothing but the sign, the exponent and the top four mantissa bits of x:
+// bits 31..19.  Ties to even also need to know whether bits 18..0 are all
+// zero (only then can x sit exactly halfway).
 #pragma once
 #include <stdint.h>
 
@@ -29,31 +31,43 @@ constexpr uint32_t kMaxBits = 0x47000000u;     // 2^15, the largest finite value
 constexpr uint32_t kOvfBits = 0x47200000u;     // 1.25 * 2^15, midpoint towards Inf
 constexpr uint32_t kMinBits = 0x34800000u;     // 2^-22, the smallest nonzero value
 
-// fp32 bit pattern of the HiF8 value nearest to x (ties away from zero).
+// fp32 bit pattern of the HiF8 value nearest to x (ties away from zero, or
+// with even to the neighbour whose significand is even: an even multiple of
+// the spacing between the two neighbours, which sends a tie between the last
+// value of a binade and the next power of two, and every tie among the
+// powers of two below 2^-15, up, and the tie between 0 and 2^-22 down).
 // saturate: finite values beyond 2^15 clamp to +-2^15 (else they round to
-// +-Inf from 1.25 * 2^15 up).  +-Inf stays +-Inf, NaN stays NaN, and values
-// that round to zero give +0.
-HIF8_HD uint32_t round_bits(uint32_t x, bool saturate)
+// +-Inf from the midpoint 1.25 * 2^15 up; at the midpoint itself, ties to
+// even keep 2^15).  +-Inf stays +-Inf, NaN stays NaN, and values that round
+// to zero give +0.
+HIF8_HD uint32_t round_bits(uint32_t x, bool saturate, bool even = false)
 {
     const uint32_t s = x & 0x80000000u;
     const uint32_t a = x & 0x7fffffffu;
     if (a >= 0x7f800000u) return x;                        // Inf, NaN
     const int e = (int)(a >> 23) - 127;
     if (e >= 15) {
-        if (saturate || a < kOvfBits) return s | kMaxBits;
+        if (saturate || a < kOvfBits || (even && a == kOvfBits)) return s | kMaxBits;
         return s | 0x7f800000u;
     }
     if (e < -23) return 0u;
-    if (e == -23) return s | kMinBits;                     // [2^-23, 2^-22) -> 2^-22
+    if (e == -23) return (even && a == 0x34000000u) ? 0u : (s | kMinBits);   // [2^-23, 2^-22) -> 2^-22
     const int ae = e < 0 ? -e : e;
     // mantissa bits kept: 3, 2, 1, or 0 (powers of two below 2^-15)
     const int w = e < -15 ? 0 : (ae <= 3 ? 3 : (ae <= 7 ? 2 : 1));
     const uint32_t half = 1u << (22 - w);
     const uint32_t keep = ~((1u << (23 - w)) - 1u);
-    return s | ((a + half) & keep);                        // a carry lands on 2^(e+1)
+    // ties to even: one less than half, plus the last kept bit (w = 0: the
+    // significand 2 is the even one, so a tie always goes up)
+    const uint32_t odd = w == 0 ? 1u : (a >> (23 - w)) & 1u;
+    const uint32_t add = even ? half - 1u + odd : half;
+    return s | ((a + add) & keep);                         // a carry lands on 2^(e+1)
 }
 
-HIF8_HD float round(float x, bool saturate = true) { return u2f(round_bits(f2u(x), saturate)); }
+HIF8_HD float round(float x, bool saturate = true, bool even = false)
+{
+    return u2f(round_bits(f2u(x), saturate, even));
+}
 
 // Code of a value that is already a HiF8 value (output of round_bits).
 HIF8_HD uint8_t code_of_rounded(uint32_t r)
@@ -77,7 +91,10 @@ HIF8_HD uint8_t code_of_rounded(uint32_t r)
     return (uint8_t)(s | c);
 }
 
-HIF8_HD uint8_t encode(float x, bool saturate = true) { return code_of_rounded(round_bits(f2u(x), saturate)); }
+HIF8_HD uint8_t encode(float x, bool saturate = true, bool even = false)
+{
+    return code_of_rounded(round_bits(f2u(x), saturate, even));
+}
 
 // Value of a code.  0x80 is NaN, 0x6F/0xEF are +-Inf, 0x00 is zero.
 HIF8_HD float decode(uint8_t code)

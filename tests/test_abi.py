@@ -141,3 +141,33 @@ def test_fp8_argument_checks(lib):
     assert ex(baps.BAPS_QK_FP8_E4M3, float("inf"), 1.0) == 1
     assert ex(baps.BAPS_QK_FP8_E4M3, 1.0, 1.0, R=4) == 2
     assert baps.baps_attention_split_workspace(1, 32, 8, 1, 32768, 128, 128, qk_scales=(1.0, 1.0)) > 0
+
+
+def test_cast_and_output_knob_checks(lib):
+    """tie_mode, saturate and out_bf16 of baps_params_t (no GPU work: the
+    checks run before any HIP call, or the work is empty)."""
+    def ex(tie=0, sat=1, out_bf16=0, lam=1, mode=0, R=1, fmt=0, B=1, o=16):
+        prm = baps.baps_params_t(lam, 1, 0.0, None, mode, R, 0, None, fmt, 1.0, 1.0, tie, sat, out_bf16)
+        return lib.baps_attention_fwd_ex(16, 16, 16, o, None, B, 8, 2, 64, 64, 128, 1, 128, ctypes.byref(prm), None)
+    assert ex(tie=2) == 1 and ex(tie=-1) == 1                       # unknown tie rule
+    assert ex(tie=1, mode=baps.BAPS_MODE_DEFAULT) == 2               # ties to even: Alg. 1 only
+    assert ex(tie=1, lam=9) == 2                                     # ... with the compact table
+    assert ex(tie=1, R=4) == 2                                       # ... per row
+    assert ex(tie=1, fmt=baps.BAPS_QK_FP8_E4M3) == 2                 # ... bf16 Q/K
+    assert ex(tie=1, B=0) == 0                                       # empty work first
+    assert ex(sat=0, lam=16) == 2                                    # an 8-bit P could overflow
+    assert ex(sat=0, lam=15, B=0) == 0 and ex(sat=0, lam=100, mode=baps.BAPS_MODE_DEFAULT, B=0) == 0
+    assert ex(out_bf16=1, o=18) == 1                                 # misaligned output
+    # the split-key path keeps the canonical ties; other knobs go to the one-pass kernels
+    assert baps.baps_attention_split_workspace(1, 32, 8, 1, 32768, 128, 128, tie_mode=1) == 0
+    assert baps.baps_attention_split_workspace(1, 32, 8, 1, 32768, 128, 128, out_bf16=True) > 0
+    assert lib.hif8_encode(16, 16, 10, baps.BAPS_HIF8_TIES_EVEN | 4, None) == 1
+
+
+def test_dump_argument_checks(lib):
+    d = lib.baps_attention_fwd_dump
+    assert d(16, 16, 16, 16, None, 1, 2, 1, 8, 8, 64, 0, 64, None, None, 16, 16, None) == 1     # no row map
+    assert d(16, 16, 16, 16, None, 1, 2, 1, 8, 8, 64, 0, 64, None, 16, None, 16, None) == 1     # no acc buffer
+    assert d(16, 16, 16, 16, None, 1, 2, 1, 8, 8, 64, 0, 64, None, 16, 16, None, None) == 1     # no ref buffer
+    assert d(16, 16, 16, 16, None, 1, 2, 1, 8, 8, 96, 0, 64, None, 16, 16, 16, None) == 2       # D
+    assert d(16, 16, 16, 16, None, 0, 2, 1, 8, 8, 64, 0, 64, None, None, None, None, None) == 0  # empty

@@ -97,8 +97,12 @@ def test_zero_keys():
     assert torch.all(o == 0) and torch.all(torch.isneginf(lse))
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4])
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
 def test_workload_sampled_rows(cfg):
+    # the full-size workloads in the benchmark's launch configuration: every
+    # row of workloads 1 and 3, and every 64th query row of every head plus
+    # the last row of each 128-row query tile of workloads 2, 4 and 5
+    # (3072, 12288 and 24576 rows)
     w, q, k, v = make_workload(cfg)
     shape = (w.B, w.Hq, w.Hkv, w.Sq, w.Sk, w.D, w.causal)
     if cfg == 1:
@@ -106,12 +110,5 @@ def test_workload_sampled_rows(cfg):
     elif cfg == 3:
         rows = sample_rows(w, every=1, tile=1)            # every decode row
     else:
-        rows = sample_rows(w, every=256, tile=512, heads=range(0, w.Hq, 3))
-    _check(q, k, v, shape, w.block, rows=rows, label=w.name)
-
-
-def test_long_prefill_sampled_rows():
-    w, q, k, v = make_workload(5)
-    shape = (w.B, w.Hq, w.Hkv, w.Sq, w.Sk, w.D, w.causal)
-    rows = sample_rows(w, every=4096, tile=8192, heads=(0, 13, 31))
+        rows = sample_rows(w, every=64, tile=128)
     _check(q, k, v, shape, w.block, rows=rows, label=w.name)

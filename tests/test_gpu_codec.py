@@ -10,7 +10,7 @@ import oracle as O
 pytestmark = pytest.mark.gpu
 
 
-def _encode_patterns(start, n, saturate):
+def _encode_patterns(start, n, saturate, even=False):
     import torch
     import paper_2602_02071_amd as baps
     bits = torch.arange(start, start + n, dtype=torch.int64, device="cuda:0")
@@ -18,22 +18,23 @@ def _encode_patterns(start, n, saturate):
     x = bits.to(torch.int32).view(torch.float32)                        # fp32 pattern start + i
     del bits
     codes = torch.empty(n, dtype=torch.uint8, device="cuda:0")
-    baps.hif8_encode(x, codes, n, baps.BAPS_HIF8_SATURATE if saturate else 0)
+    flags = (baps.BAPS_HIF8_SATURATE if saturate else 0) | (baps.BAPS_HIF8_TIES_EVEN if even else 0)
+    baps.hif8_encode(x, codes, n, flags)
     torch.cuda.synchronize()
     return codes.cpu().numpy()
 
 
-@pytest.mark.parametrize("saturate", [True, False])
-def test_encode_every_fp32_pattern(saturate):
+@pytest.mark.parametrize("saturate,even", [(True, False), (False, False), (True, True), (False, True)])
+def test_encode_every_fp32_pattern(saturate, even):
     chunk = 1 << 28
     total = 1 << 32
     # the non-saturating mode differs only near and beyond 2^15: a stride of chunks suffices there
     starts = range(0, total, chunk) if saturate else range(0, total, 4 * chunk)
     for start in starts:
-        codes = _encode_patterns(start, chunk, saturate)
-        bad, first = O.check_patterns(start, codes, saturate)
+        codes = _encode_patterns(start, chunk, saturate, even)
+        bad, first = O.check_patterns(start, codes, saturate, ties_even=even)
         assert bad == 0, f"{bad} mismatches from pattern {start:#x}, first at {start + first:#x}"
-    print(f"encode saturate={saturate}: {len(starts) * chunk} patterns bit-exact", flush=True)
+    print(f"encode saturate={saturate} even={even}: {len(starts) * chunk} patterns bit-exact", flush=True)
 
 
 def test_encode_ragged_unaligned():
@@ -51,6 +52,13 @@ def test_encode_ragged_unaligned():
         torch.cuda.synchronize()
         got = buf[off_c:off_c + n].cpu().numpy()
         assert np.array_equal(got, want[off_x:])
+    # ties to even on the unaligned (scalar) kernel, with ties present
+    xt2 = torch.from_numpy(np.concatenate([x, np.float32([1.0625, 22.0, 2.0 ** -23, -10.0])])).to("cuda:0")
+    want2 = O.hif8_encode(xt2.cpu().numpy(), ties_even=True)
+    baps.hif8_encode(xt2.data_ptr() + 4, buf.data_ptr() + 1, xt2.numel() - 1,
+                     baps.BAPS_HIF8_SATURATE | baps.BAPS_HIF8_TIES_EVEN)
+    torch.cuda.synchronize()
+    assert np.array_equal(buf[1:xt2.numel()].cpu().numpy(), want2[1:])
 
 
 def test_decode_all_codes_and_lut():
