@@ -191,6 +191,25 @@ int baps_attention_fwd_split(const void* q, const void* k, const void* v, float*
                              void* stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation):
+ * baps_attention_fwd_split with the workspace taken from the library's own
+ * static device scratch of BAPS_SPLIT_SCRATCH_BYTES (32 MiB, one copy per
+ * device, held until the process ends) instead of a caller's buffer.  The
+ * call allocates nothing.  Same arguments, results and kernels as
+ * baps_attention_fwd_split; shapes that take the one-pass kernels run them
+ * (no scratch).  BAPS_UNSUPPORTED when the shape's workspace
+ * (baps_attention_split_workspace) exceeds BAPS_SPLIT_SCRATCH_BYTES.  Every
+ * call on a device shares that device's scratch: calls that overlap on one
+ * GPU (other streams, other threads) race and must be serialised by the
+ * caller; the scratch needs no clearing (its contents are undefined on entry).
+ */
+#define BAPS_SPLIT_SCRATCH_BYTES (32LL << 20)
+int baps_attention_fwd_split_noalloc(const void* q, const void* k, const void* v, float* o, float* lse,
+                                     int B, int Hq, int Hkv, int Sq, int Sk, int D, int causal, int block,
+                                     const baps_params_t* p, void* stream);
+
+/*
  * HiF8 codec (the 8-bit format used by every 8-bit step of the method;
  * Sec. 2, App. A).  hif8_encode: codes[i] = code of the HiF8 value nearest
  * to x[i].  flags: BAPS_HIF8_SATURATE clamps finite overflow to +-2^15 (else

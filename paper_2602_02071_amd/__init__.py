@@ -22,7 +22,10 @@ BAPS_HIF8_TIES_EVEN = 2
 BAPS_TIES_AWAY = 0
 BAPS_TIES_EVEN = 1
 
+BAPS_SPLIT_SCRATCH_BYTES = 32 << 20
+
 EXPORTS = ("baps_attention_fwd", "baps_attention_fwd_ex", "baps_attention_fwd_split", "baps_attention_fwd_dump",
+           "baps_attention_fwd_split_noalloc",
            "hif8_encode", "hif8_decode", "baps_softmax_block", "baps_get_exp2_lut", "baps_init",
            "baps_attention_split_workspace", "baps_last_hip_error", "baps_status_string")
 
@@ -74,6 +77,8 @@ def load():
                                            ctypes.POINTER(baps_params_t), P, LL, P]
     L.baps_attention_fwd_dump.argtypes = [P, P, P, P, P, I, I, I, I, I, I, I, I,
                                           ctypes.POINTER(baps_params_t), P, P, P, P]
+    L.baps_attention_fwd_split_noalloc.argtypes = [P, P, P, P, P, I, I, I, I, I, I, I, I,
+                                                   ctypes.POINTER(baps_params_t), P]
     L.baps_attention_split_workspace.argtypes = [I, I, I, I, I, I, I, ctypes.POINTER(baps_params_t)]
     L.hif8_encode.argtypes = [P, P, LL, I, P]
     L.hif8_decode.argtypes = [P, P, LL, P]
@@ -172,6 +177,15 @@ def baps_attention_fwd_split(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, blo
     _check("baps_attention_fwd_split", load().baps_attention_fwd_split(
         _p(q), _p(k), _p(v), _p(o), _p(lse), B, Hq, Hkv, Sq, Sk, D, int(causal), block,
         ctypes.byref(prm), _p(workspace), int(workspace_bytes), _stream(stream)))
+
+
+def baps_attention_fwd_split_noalloc(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, stream=None, **knobs):
+    """The split-key path on the library's static scratch (no allocation);
+    knobs as baps_attention_fwd_ex."""
+    prm = _params(**knobs)
+    _check("baps_attention_fwd_split_noalloc", load().baps_attention_fwd_split_noalloc(
+        _p(q), _p(k), _p(v), _p(o), _p(lse), B, Hq, Hkv, Sq, Sk, D, int(causal), block,
+        ctypes.byref(prm), _stream(stream)))
 
 
 def hif8_encode(x, codes, n, flags=BAPS_HIF8_SATURATE, stream=None):

@@ -98,6 +98,14 @@ const Table& host_table()
 
 constexpr int kMaxDevices = 64;
 std::mutex g_mutex;
+
+// Scratch of baps_attention_fwd_split_noalloc: the split-key workspace in
+// static device memory, one copy per device (held until the process ends).
+// In host code this name is a host-side stand-in, never a device address:
+// g_dev_scratch[dev] holds the device's own address of it, taken once per
+// device with that device current.
+static __device__ __attribute__((aligned(256))) char scratch[BAPS_SPLIT_SCRATCH_BYTES];
+void* g_dev_scratch[kMaxDevices] = {};
 const uint32_t* g_dev_table[kMaxDevices] = {};
 const uint8_t* g_dev_code[kMaxDevices] = {};
 const uint8_t* g_dev_codex[kMaxDevices] = {};
@@ -134,6 +142,7 @@ int upload(const void* symbol, const T (&host)[N], const void** dev_addr)
 struct DevTables {
     const uint32_t* tab;
     const uint8_t *code, *codex, *code_even, *codex_even;
+    void* scratch;
 };
 
 int table_on_current_device(const uint32_t** out, const uint8_t** code = nullptr, const uint8_t** codex = nullptr,
@@ -164,6 +173,10 @@ int table_on_current_device(const uint32_t** out, const uint8_t** code = nullptr
         const void *eptr = nullptr, *exptr = nullptr;
         if (int st = upload(HIP_SYMBOL(g_code_table_even), t.code_even, &eptr)) return st;
         if (int st = upload(HIP_SYMBOL(g_code_table_x_even), t.codex_even, &exptr)) return st;
+        void* sptr = nullptr;
+        if (int st = status_of(hipGetSymbolAddress(&sptr, HIP_SYMBOL(scratch)))) return st;
+        if (!sptr) return BAPS_HIP_ERROR;
+        g_dev_scratch[dev] = sptr;
         g_dev_code_even[dev] = static_cast<const uint8_t*>(eptr);
         g_dev_codex_even[dev] = static_cast<const uint8_t*>(exptr);
         g_dev_code[dev] = static_cast<const uint8_t*>(cptr);
@@ -174,7 +187,7 @@ int table_on_current_device(const uint32_t** out, const uint8_t** code = nullptr
     if (code) *code = g_dev_code[dev];
     if (codex) *codex = g_dev_codex[dev];
     if (all) *all = DevTables{g_dev_table[dev], g_dev_code[dev], g_dev_codex[dev], g_dev_code_even[dev],
-                              g_dev_codex_even[dev]};
+                              g_dev_codex_even[dev], g_dev_scratch[dev]};
     return BAPS_OK;
 }
 
@@ -351,6 +364,38 @@ SplitPlan split_plan(int B, int Hq, int Hkv, int Sq, int Sk, int D, int block, c
     return sp;
 }
 
+// The split-key path of a call whose plan uses it.  workspace == nullptr
+// takes the device's static scratch (the caller has checked the size).
+int split_impl(const void* q, const void* k, const void* v, float* o, float* lse, int B, int Hq, int Hkv,
+               int Sq, int Sk, int D, int causal, int block, const baps_params_t& kn, const SplitPlan& plan,
+               void* workspace, long long workspace_bytes, void* stream)
+{
+    SplitParams sp;
+    bool empty = false;
+    int st = make_params(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, kn, &sp.a, &empty);
+    if (st || empty) return st;
+    if (workspace && (workspace_bytes < plan.bytes || ((uintptr_t)workspace & 255u))) return BAPS_INVALID_ARGUMENT;
+    DevTables t{};
+    const uint32_t* tab = nullptr;
+    if ((st = table_on_current_device(&tab, nullptr, nullptr, &t))) return st;
+    sp.a.tab = t.tab;
+    sp.a.ctab = t.code;
+    sp.a.ctabx = t.codex;
+    sp.a.ctab_even = t.code_even;
+    sp.a.ctabx_even = t.codex_even;
+    if (!workspace) workspace = t.scratch;
+    char* ws = static_cast<char*>(workspace);
+    sp.acc = reinterpret_cast<float*>(ws + plan.off_acc);
+    sp.bmax = reinterpret_cast<float*>(ws + plan.off_bmax);
+    sp.part = reinterpret_cast<float*>(ws + plan.off_part);
+    sp.nblk = plan.nblk;
+    sp.bstride = plan.bstride;
+    sp.nsplit = plan.nsplit;
+    sp.bps = plan.bps;
+    clear_stale_error();
+    return status_of(launch_attention_split(sp, D, block, static_cast<hipStream_t>(stream)));
+}
+
 }  // namespace
 
 extern "C" {
@@ -370,22 +415,24 @@ int baps_attention_fwd_split(const void* q, const void* k, const void* v, float*
         const baps_params_t kn = knobs_of(prm);
         const SplitPlan plan = split_plan(B, Hq, Hkv, Sq, Sk, D, block, kn);
         if (!plan.use) return attention_impl(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, kn, stream);
-        SplitParams sp;
-        bool empty = false;
-        int st = make_params(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, kn, &sp.a, &empty);
-        if (st || empty) return st;
-        if (!workspace || workspace_bytes < plan.bytes || ((uintptr_t)workspace & 255u)) return BAPS_INVALID_ARGUMENT;
-        if ((st = attach_tables(&sp.a))) return st;
-        char* ws = static_cast<char*>(workspace);
-        sp.acc = reinterpret_cast<float*>(ws + plan.off_acc);
-        sp.bmax = reinterpret_cast<float*>(ws + plan.off_bmax);
-        sp.part = reinterpret_cast<float*>(ws + plan.off_part);
-        sp.nblk = plan.nblk;
-        sp.bstride = plan.bstride;
-        sp.nsplit = plan.nsplit;
-        sp.bps = plan.bps;
-        clear_stale_error();
-        return status_of(launch_attention_split(sp, D, block, static_cast<hipStream_t>(stream)));
+        if (!workspace) return BAPS_INVALID_ARGUMENT;
+        return split_impl(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, kn, plan, workspace,
+                          workspace_bytes, stream);
+    } catch (...) {
+        return BAPS_HIP_ERROR;
+    }
+}
+
+int baps_attention_fwd_split_noalloc(const void* q, const void* k, const void* v, float* o, float* lse, int B,
+                                     int Hq, int Hkv, int Sq, int Sk, int D, int causal, int block,
+                                     const baps_params_t* prm, void* stream)
+{
+    try {
+        const baps_params_t kn = knobs_of(prm);
+        const SplitPlan plan = split_plan(B, Hq, Hkv, Sq, Sk, D, block, kn);
+        if (!plan.use) return attention_impl(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, kn, stream);
+        if (plan.bytes > BAPS_SPLIT_SCRATCH_BYTES) return BAPS_UNSUPPORTED;
+        return split_impl(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, D, causal, block, kn, plan, nullptr, 0, stream);
     } catch (...) {
         return BAPS_HIP_ERROR;
     }
