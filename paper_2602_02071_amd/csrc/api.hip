@@ -112,6 +112,7 @@ const uint8_t* g_dev_codex[kMaxDevices] = {};
 const uint8_t* g_dev_code_even[kMaxDevices] = {};
 const uint8_t* g_dev_codex_even[kMaxDevices] = {};
 
+
 // the last HIP failure a call of this library met on the calling thread
 thread_local hipError_t g_last_hip = hipSuccess;
 
@@ -177,6 +178,7 @@ int table_on_current_device(const uint32_t** out, const uint8_t** code = nullptr
         if (int st = status_of(hipGetSymbolAddress(&sptr, HIP_SYMBOL(scratch)))) return st;
         if (!sptr) return BAPS_HIP_ERROR;
         g_dev_scratch[dev] = sptr;
+
         g_dev_code_even[dev] = static_cast<const uint8_t*>(eptr);
         g_dev_codex_even[dev] = static_cast<const uint8_t*>(exptr);
         g_dev_code[dev] = static_cast<const uint8_t*>(cptr);
@@ -192,6 +194,27 @@ int table_on_current_device(const uint32_t** out, const uint8_t** code = nullptr
 }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// The least fp32 value T with ceil(HiF8(T)) > lambda (ties away), -inf when
+// every T has it: ceil(HiF8(.)) does not decrease with T, so a binary search
+// over the fp32 values in order finds the step.  Alg. 1 restarts a block in
+// B1 exactly when the 8-bit T of its row maximum reaches it.
+float restart_threshold(int lambda)
+{
+    auto key_value = [](uint32_t key) {              // key order = value order over all non-NaN fp32
+        const uint32_t bits = (key & 0x80000000u) ? (key & 0x7fffffffu) : ~key;
+        return hif8::u2f(bits);
+    };
+    auto above = [&](uint32_t key) { return std::ceil(hif8::round(key_value(key), true)) > (float)lambda; };
+    uint32_t lo = 0x007fffffu, hi = 0xff800000u;      // keys of -inf and +inf
+    if (above(lo)) return -INFINITY;
+    if (!above(hi)) return INFINITY;
+    while (hi - lo > 1) {                             // above(lo) false, above(hi) true
+        const uint32_t mid = lo + (hi - lo) / 2;
+        if (above(mid)) hi = mid; else lo = mid;
+    }
+    return key_value(hi);
+}
 
 
 // Canonical knobs when the caller passes none.
@@ -265,6 +288,7 @@ int make_params(const void* q, const void* k, const void* v, float* o, float* ls
     p.tab = nullptr;
     p.ctab = nullptr;
     p.ctabx = nullptr;
+    p.dec_x0 = restart_threshold(kn.lambda);
     p.q = static_cast<const uint16_t*>(q);
     p.k = static_cast<const uint16_t*>(k);
     p.v = static_cast<const uint16_t*>(v);
@@ -304,6 +328,7 @@ int attach_tables(AttnParams* p)
     p->tab = t.tab;
     p->ctab = t.code;
     p->ctabx = t.codex;
+
     p->ctab_even = t.code_even;
     p->ctabx_even = t.codex_even;
     return st;
@@ -381,6 +406,7 @@ int split_impl(const void* q, const void* k, const void* v, float* o, float* lse
     sp.a.tab = t.tab;
     sp.a.ctab = t.code;
     sp.a.ctabx = t.codex;
+
     sp.a.ctab_even = t.code_even;
     sp.a.ctabx_even = t.codex_even;
     if (!workspace) workspace = t.scratch;

@@ -309,6 +309,10 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
     // expanded to all 8192 indices (no lookup needs a clamp); else the bf16
     // half of the full score table
     __shared__ __attribute__((aligned(1024))) uint8_t ctab[CT ? (TIE ? 2 : 1) * kTabEntries : 1];
+    // restart test of Alg. 1 against the threshold T >= dec_x0 and the
+    // branch-free increment (CT kernels with ties away: lambda <= 8); the
+    // others round T in registers
+    constexpr bool kDec = CT && MODE == kModeE2E && !TIE;
     __shared__ __attribute__((aligned(16))) uint16_t tab[CT ? 1 : kTabEntries];
     __shared__ uint32_t tflag[TILE ? NW : 1][3];  // per wave: rows that restart, see the block, are in B0
     extern __shared__ __attribute__((aligned(1024))) char tiles[];
@@ -629,8 +633,18 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
                 const bool vis = (!TILE || row_ok) && amax != ninf;
                 const bool in_b0 = (jb < p.n_b0) || (p.b0_last && jb == kmax / BLK);
                 const bool forced = in_b0 || (m == ninf);
-                const float tq = hif8::round(__builtin_fmaf(amax, c, -m), true, TIE);
-                bool restart = forced || (ceilf(tq) > lam);
+                // ceil(rowmax T) of the 8-bit T = fl32(acc*c - m): the 8-bit cast
+                // of the raw maximum's T (the cast is monotone), then ceil
+                const float xt = __builtin_fmaf(amax, c, -m);
+                float ctq;
+                bool restart;
+                if constexpr (kDec) {
+                    restart = forced || (xt >= p.dec_x0);
+                    ctq = hif8_ceil_below9(xt);            // used only without a restart
+                } else {
+                    ctq = ceilf(hif8::round(xt, true, TIE));
+                    restart = forced || (ctq > lam);
+                }
                 if constexpr (TILE) {
                     // the tile restarts when any of its rows that see the block would
                     const uint32_t wantb = (uint32_t)__ballot(vis && restart);
@@ -669,7 +683,7 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
                     n_restart += (b1 && restart) ? 1u : 0u;
                 }
                 const float m_hi = __builtin_fmaxf(m, ceilf(amax * c));    // ceil(rowmax S), S in fp32
-                const float m_new = vis ? (restart ? m_hi : m + __builtin_fmaxf(0.0f, ceilf(tq))) : m;
+                const float m_new = vis ? (restart ? m_hi : m + __builtin_fmaxf(0.0f, ctq)) : m;
                 const float ref_new = vis ? (restart ? m_hi : m) : ref;
                 const float f = (ref == ninf) ? 1.0f : exp2_int(ref - ref_new);
                 if (__any(f != 1.0f)) {

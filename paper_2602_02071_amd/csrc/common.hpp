@@ -58,6 +58,21 @@ constexpr int kCodeTableBytes = (kCodeEntries + 1023) / 1024 * 1024;   // device
 constexpr int kCodeBiasLog2 = 104;
 constexpr int kCodeMaxLambda = 8;
 
+// max(0, ceil(HiF8(x))) (ties away) for x below 8.75, branch-free: below
+// 2^-23 the cast gives 0 or less; up to 1 it gives a value in (0, 1]; from 1
+// up to 16 it keeps 3 mantissa bits, so every integer k is a HiF8 value and
+// x in (k, k + h) (h half the spacing, 2^(e-4) in binade [2^e, 2^(e+1)))
+// rounds down to k, while x from k + h up rounds above k.  Alg. 1's increment
+// of the integer maximum when a block does not restart (T <= lambda <= 8).
+__device__ __forceinline__ float hif8_ceil_below9(float x)
+{
+    const float fl = floorf(x), ce = ceilf(x);
+    const float h = hif8::u2f((hif8::f2u(x) & 0x7f800000u) - (4u << 23));
+    const float fr = x - fl;                                  // exact
+    const float r = (fr > 0.0f && fr < h) ? fl : ce;
+    return x < 1.0f ? (x >= 0x1p-23f ? 1.0f : 0.0f) : r;
+}
+
 // Softmax setups of the fused attention kernels: the proposed workflow
 // (Alg. 1, "E2E HiF8") and two setups of eq. (2) with a real-valued running
 // maximum, "Default" (fp32 exp2) and "Exp2 HiF8" (the exp2 evaluated on 8-bit
@@ -75,6 +90,8 @@ struct AttnParams {
     const uint32_t* tab;        // score table (device)
     const uint8_t* ctab;        // compact code table (device), kCodeTableBytes bytes (entries, then zeros)
     const uint8_t* ctabx;       // the compact code table expanded to all kTabEntries indices (device)
+    float dec_x0;               // the least fp32 T with ceil(HiF8(T)) > lambda (ties away): Alg. 1's
+                                // restart test is T >= dec_x0
     unsigned long long* counters;  // [B*Hq][2] restarted / visited B1 tile-blocks, or null
     unsigned long long* tile_counts;  // [B*Hq][ceil(Sq/R)][2] the same per tile, or null
     int B, Hq, Hkv, Sq, Sk;
