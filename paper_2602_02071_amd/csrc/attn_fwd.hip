@@ -471,6 +471,7 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
     const float ninf = -__builtin_huge_valf();
     const float c = p.c;
     const float lam = (float)p.lambda;
+    const bool count_blocks = p.counters || p.tile_counts;   // restart / visit counts requested
     int sel = 0;                        // K/V buffer of the current key block
 
     for (int rnd = 0;; ++rnd) {
@@ -677,15 +678,20 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
                         ++n_visit;
                         n_restart += restart ? 1u : 0u;
                     }
-                } else {
+                } else if (count_blocks) {
                     const bool b1 = vis && !in_b0;
                     n_visit += b1 ? 1u : 0u;
                     n_restart += (b1 && restart) ? 1u : 0u;
                 }
                 const float m_hi = __builtin_fmaxf(m, ceilf(amax * c));    // ceil(rowmax S), S in fp32
-                const float m_new = vis ? (restart ? m_hi : m + __builtin_fmaxf(0.0f, ctq)) : m;
+                // (kDec, per row: a row that does not see the block has amax =
+                // -inf, so T = -inf (m finite: no restart unless forced, ctq = 0)
+                // or m = -inf (forced: m_hi = m), and m stays as it is)
+                const float m_new = (kDec && !TILE) ? (restart ? m_hi : m + ctq)
+                                                    : (vis ? (restart ? m_hi : m + __builtin_fmaxf(0.0f, ctq)) : m);
                 const float ref_new = vis ? (restart ? m_hi : m) : ref;
-                const float f = (ref == ninf) ? 1.0f : exp2_int(ref - ref_new);
+                // (ref_new >= ref: the reference never decreases)
+                const float f = (ref == ninf) ? 1.0f : exp2_nonpos_int(ref - ref_new);
                 if (__any(f != 1.0f)) {
         #pragma unroll
                     for (int t = 0; t < kDT; ++t)

@@ -59,18 +59,24 @@ constexpr int kCodeBiasLog2 = 104;
 constexpr int kCodeMaxLambda = 8;
 
 // max(0, ceil(HiF8(x))) (ties away) for x below 8.75, branch-free: below
-// 2^-23 the cast gives 0 or less; up to 1 it gives a value in (0, 1]; from 1
-// up to 16 it keeps 3 mantissa bits, so every integer k is a HiF8 value and
-// x in (k, k + h) (h half the spacing, 2^(e-4) in binade [2^e, 2^(e+1)))
-// rounds down to k, while x from k + h up rounds above k.  Alg. 1's increment
-// of the integer maximum when a block does not restart (T <= lambda <= 8).
+// 2^-23 the cast gives 0 or less; from 2^-23 up to 16 it keeps at most 3
+// mantissa bits, so with h half the spacing of x's binade (2^(e-4) in
+// [2^e, 2^(e+1)) for e >= 0, below the spacing for e < 0) the cast exceeds an
+// integer k exactly when x >= k + h (ties go away from zero), and
+// ceil(HiF8(x)) = floor(x - h) + 1; x - h is exact (h is at least one unit in
+// the last place of x).  Alg. 1's increment of the integer maximum when a
+// block does not restart (T <= lambda <= 8).
 __device__ __forceinline__ float hif8_ceil_below9(float x)
 {
-    const float fl = floorf(x), ce = ceilf(x);
     const float h = hif8::u2f((hif8::f2u(x) & 0x7f800000u) - (4u << 23));
-    const float fr = x - fl;                                  // exact
-    const float r = (fr > 0.0f && fr < h) ? fl : ce;
-    return x < 1.0f ? (x >= 0x1p-23f ? 1.0f : 0.0f) : r;
+    const float r = floorf(x - h) + 1.0f;
+    return x >= 0x1p-23f ? r : 0.0f;
+}
+
+// 2^k for an integer-valued k <= 0 (0 below the fp32 range)
+__device__ __forceinline__ float exp2_nonpos_int(float k)
+{
+    return ldexpf(1.0f, (int)__builtin_fmaxf(k, -200.0f));
 }
 
 // Softmax setups of the fused attention kernels: the proposed workflow
