@@ -31,7 +31,8 @@
 //     O^T += V_j^T P^T once the keys inside each 16-key group are taken in a
 //     fixed permuted order; the A operand (V^T fragments) comes straight from
 //     the [key][d] tile through ds_read_b64_tr_b16 transposing reads, in the
-//     same key order.  P never leaves registers.  The softmax of 32-key tile
+//     same key order.  P never leaves registers.  The table reads of the
+//     whole block are issued ahead of the PV loop; the packing of 32-key tile
 //     t+1 runs on the VALU while the PV MFMAs of tile t execute.
 #include "common.hpp"
 
@@ -739,6 +740,25 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
     
             if (!live) continue;
             const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+            // T and the table entry of every score of the block first, written
+            // ahead of the PV loop so that the gathers are in flight well
+            // before the packing that reads them (T = fl32(acc*c - ref) rounded
+            // once for Alg. 1; fl32(S - m) with S = fl32(acc*c) for Exp2 HiF8;
+            // under ties to even a T with bits 18..0 zero reads the second half
+            // of the table)
+            uint32_t cd[kKT][16];
+            if constexpr (MODE != kModeDefault) {
+#pragma unroll
+                for (int kt = 0; kt < kKT; ++kt)
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) {
+                        const float t = MODE == kModeE2E ? __builtin_fmaf(sacc[kt][i], c, nref) : sacc[kt][i] * c + nref;
+                        const uint32_t u = hif8::f2u(t);
+                        uint32_t idx = u >> kTabShift;
+                        if constexpr (TIE) idx |= (u & 0x7ffffu) ? 0u : (uint32_t)kTabEntries;
+                        cd[kt][i] = CT ? (uint32_t)ctab[idx] : (uint32_t)tab[idx];
+                    }
+            }
 #pragma unroll
             for (int kt = 0; kt < kKT; ++kt) {
                 // P = HiF8(2^HiF8(T)), T = fl32(acc*c - ref), for this 32-key tile,
@@ -759,24 +779,9 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
                             pop[ch][e] = w;
                             continue;
                         }
-                        // T = fl32(acc*c - ref) rounded once (Alg. 1), or fl32(S - m) with
-                        // S = fl32(acc*c) (eq. (2), Exp2 HiF8)
-                        const float t0 = MODE == kModeE2E ? __builtin_fmaf(sacc[kt][ch * 8 + 2 * e], c, nref)
-                                                          : sacc[kt][ch * 8 + 2 * e] * c + nref;
-                        const float t1 = MODE == kModeE2E ? __builtin_fmaf(sacc[kt][ch * 8 + 2 * e + 1], c, nref)
-                                                          : sacc[kt][ch * 8 + 2 * e + 1] * c + nref;
-                        if constexpr (TIE) {
-                            // a T with bits 18..0 zero reads the ties-to-even half of the table
-                            const uint32_t u0 = hif8::f2u(t0), u1 = hif8::f2u(t1);
-                            const uint32_t i0 = (u0 >> kTabShift) | ((u0 & 0x7ffffu) ? 0u : (uint32_t)kTabEntries);
-                            const uint32_t i1 = (u1 >> kTabShift) | ((u1 & 0x7ffffu) ? 0u : (uint32_t)kTabEntries);
-                            w = ((uint32_t)ctab[i0] | ((uint32_t)ctab[i1] << 16)) << 4;
-                        } else if constexpr (CT) {
-                            // two bf16 of P * 2^-kCodeBiasLog2
-                            w = ((uint32_t)ctab[hif8::f2u(t0) >> kTabShift] | ((uint32_t)ctab[hif8::f2u(t1) >> kTabShift] << 16)) << 4;
-                        } else {
-                            w = (uint32_t)tab[hif8::f2u(t0) >> kTabShift] | ((uint32_t)tab[hif8::f2u(t1) >> kTabShift] << 16);
-                        }
+                        // two bf16 of P * 2^-kCodeBiasLog2 (code table), or of P (score table)
+                        if constexpr (CT) w = (cd[kt][ch * 8 + 2 * e] | (cd[kt][ch * 8 + 2 * e + 1] << 16)) << 4;
+                        else w = cd[kt][ch * 8 + 2 * e] | (cd[kt][ch * 8 + 2 * e + 1] << 16);
                         pop[ch][e] = w;
                         dl = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), ones, dl, false);
                     }
