@@ -202,13 +202,13 @@ def fp8_qk(steps=20):
                 torch.cuda.synchronize()
                 rows = sample_rows(w, every=256, tile=512) if w.Sq > 1 else np.arange(0, w.B * w.Hq, 4)
                 qb, kb = oracle.e4m3_to_bf16(q8), oracle.e4m3_to_bf16(k8)
+                c8 = oracle.fp8_scale_log2(w.D, qs, ks)
                 ref, _, _ = oracle.attention(qb, kb, v, w.B, w.Hq, w.Hkv, w.Sq, w.Sk, w.D, w.causal, w.block,
-                                             rows=rows, scale_log2=oracle.fp8_scale_log2(w.D, qs, ks))
-                got = o.reshape(-1, w.D)[torch.as_tensor(rows, device=dev)].double().cpu().numpy()
-                rel = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
-                mx = float(np.abs(got - ref).max())
-                rec["fp8_parity"] = {"rows": int(len(rows)), "rel_l2": rel, "max_abs": mx,
-                                     "within_bar": bool(rel <= 2e-3 and mx <= 1e-2)}
+                                             rows=rows, scale_log2=c8)
+                par = parity(w, (qb, kb, v), rows, ref, (q8t, k8t, vt, o, lse), qk_scales=(qs, ks), scale_log2=c8)
+                par["within_bar"] = bool(par["rel_l2_vs_oracle"] <= 2e-3
+                                         and par["rows_past_max_abs_1e-2"] == par["of_which_match_alg1_on_kernel_scores"])
+                rec["fp8_parity"] = par
             if w.Sq > 1:
                 tf = w.flops / (us * 1e-6) / 1e12
                 peak = PEAK_BF16_TFLOPS if name == "bf16" else 1.0 / (0.5 / 5000.0 + 0.5 / PEAK_BF16_TFLOPS)
@@ -383,8 +383,11 @@ def cpu_baseline(w, qkv, gpu=None):
     return base, (parity(w, qkv, rows, ref, gpu) if gpu is not None else None)
 
 
-def parity(w, qkv, rows, ref, gpu):
-    """The GPU's O of the timed steps on `rows` against the oracle's `ref`."""
+def parity(w, qkv, rows, ref, gpu, qk_scales=None, scale_log2=0.0):
+    """The GPU's O of the timed steps on `rows` against the oracle's `ref`.
+    With FP8 Q/K, qkv holds the codes' values as bf16 patterns, gpu the
+    code tensors, and qk_scales / scale_log2 the scales and the folded score
+    scale the oracle ran with."""
     import torch
     import oracle
     import paper_2602_02071_amd as baps
@@ -392,7 +395,8 @@ def parity(w, qkv, rows, ref, gpu):
     qt, kt, vt, o, lse = gpu
     torch.cuda.synchronize()
     got = o.reshape(-1, w.D)[torch.as_tensor(rows, device=o.device)].double().cpu().numpy()
-    ex, _ = oracle.exact_attention(q, k, v, w.B, w.Hq, w.Hkv, w.Sq, w.Sk, w.D, w.causal, rows=rows)
+    ex, _ = oracle.exact_attention(q, k, v, w.B, w.Hq, w.Hkv, w.Sq, w.Sk, w.D, w.causal, rows=rows,
+                                   scale_log2=scale_log2)
     rel = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
     row_err = np.abs(got - ref).max(axis=1)
     past = np.where(row_err > 1e-2)[0]
@@ -400,10 +404,11 @@ def parity(w, qkv, rows, ref, gpu):
     if past.size:
         # the rows past 1e-2: Alg. 1 on the kernel's own scores must reproduce them
         prow = np.asarray(rows)[past]
-        _, _, acc, _ = baps.attention_dump(qt, kt, vt, w.causal, w.block, prow)
+        _, _, acc, _ = baps.attention_dump(qt, kt, vt, w.causal, w.block, prow, qk_scales=qk_scales)
         acc = acc.cpu().numpy()
         arb, _, _ = oracle.attention(q, k, v, w.B, w.Hq, w.Hkv, w.Sq, w.Sk, w.D, w.causal, w.block, rows=prow,
-                                     acc=np.where(np.isfinite(acc), acc, 0).astype(np.float32))
+                                     acc=np.where(np.isfinite(acc), acc, 0).astype(np.float32),
+                                     scale_log2=scale_log2)
         explained = int((np.abs(got[past] - arb).max(axis=1) <= 1e-4).sum())
     return {"workload": w.name, "rows": int(len(rows)), "rel_l2_vs_oracle": rel,
             "max_abs_vs_oracle": float(row_err.max()),
