@@ -119,3 +119,27 @@ def test_dump_leaves_unseen_entries_and_matches_exact_scores():
     o1, l1 = baps.attention(dev_bf16(q), dev_bf16(k), dev_bf16(v), True, block)
     torch.cuda.synchronize()
     assert torch.equal(o, o1) and torch.equal(lse, l1)
+
+
+def test_workload2_full_size_ties_even_and_bf16_o():
+    """Ties to even and bf16 O on the full Llama-3-8B-shaped prefill in the
+    benchmark's launch configuration (the persistent grid): parity of the
+    ties-to-even kernel on the sampled rows (every 64th query row of every
+    head and the last row of each 128-row tile), and bf16 O equal, bit for
+    bit, to the round-to-nearest-even of the fp32 O."""
+    import torch
+    import paper_2602_02071_amd as baps
+    from paper_2602_02071_amd.workloads import make_workload, sample_rows
+    w, q, k, v = make_workload(2)
+    shape = (w.B, w.Hq, w.Hkv, w.Sq, w.Sk, w.D, w.causal)
+    args = (dev_bf16(q), dev_bf16(k), dev_bf16(v), w.causal, w.block)
+    oe, le = baps.attention(*args, tie_mode=baps.BAPS_TIES_EVEN)
+    o32, l32 = baps.attention(*args)
+    o16, l16 = baps.attention(*args, out_bf16=True)
+    torch.cuda.synchronize()
+    assert torch.equal(o16.view(torch.int16), o32.to(torch.bfloat16).view(torch.int16))
+    assert torch.equal(l16, l32)
+    rows = sample_rows(w, every=64, tile=128)
+    oe = oe.cpu().numpy().reshape(-1, w.D)[rows].astype(np.float64)
+    le = le.cpu().numpy().reshape(-1)[rows].astype(np.float64)
+    check_parity(q, k, v, shape, w.block, oe, le, rows=rows, label=f"ties even {w.name}", tie_even=True)
