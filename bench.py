@@ -300,7 +300,8 @@ def boundary_kernels(steps=10):
     hif8_encode / hif8_decode over 2^28 elements (1 GiB of fp32, beyond the
     256 MiB Infinity Cache) and baps_softmax_block over 16384 x 8192 scores
     with 128-column blocks.  Bytes are algorithmic (each input read once,
-    each output written once)."""
+    each output written once).  A plain device copy of the same 1 GiB is
+    timed beside them as the practical streaming rate."""
     import torch
     import paper_2602_02071_amd as baps
 
@@ -317,7 +318,12 @@ def boundary_kernels(steps=10):
     res["hif8_encode"] = {"elements": n, "us": t * 1e6, "GB/s": 5 * n / t / 1e9, "frac_of_hbm_peak": 5 * n / t / 1e9 / PEAK_HBM_GBS}
     t = timed(lambda: baps.hif8_decode(codes, x, n))
     res["hif8_decode"] = {"elements": n, "us": t * 1e6, "GB/s": 5 * n / t / 1e9, "frac_of_hbm_peak": 5 * n / t / 1e9 / PEAK_HBM_GBS}
-    del x, codes
+    # context: a plain device-to-device copy of the same 1 GiB (read + write),
+    # the streaming rate the HBM sustains for a mixed read/write stream
+    y = torch.empty_like(x)
+    t = timed(lambda: y.copy_(x))
+    res["device_copy"] = {"bytes": 8 * n, "us": t * 1e6, "GB/s": 8 * n / t / 1e9, "frac_of_hbm_peak": 8 * n / t / 1e9 / PEAK_HBM_GBS}
+    del x, y, codes
     rows, cols, blk = 16384, 8192, 128
     nb = cols // blk
     s = torch.randn(rows, cols, device="cuda:0", generator=g) * 4

@@ -165,8 +165,14 @@ constexpr int kRowsPerWave4 = 4;
 // NT threads per workgroup, 4 rows per wave.  With rows enough to give every
 // CU a workgroup, 1024 threads (64 rows, one workgroup and one 32 KiB table
 // copy per CU) run about 10 % faster than 256 threads (four workgroups and
-// four table copies per CU).
-template <int BLOCK, int NT>
+// four table copies per CU).  KCH columns of a row stream per step, and the
+// next step's loads are in flight while one is processed.  256 columns keep
+// the kernel at 64 VGPRs (8 waves per SIMD), which suits grids of many
+// workgroups per CU and short rows; wider steps put more bytes in flight per
+// wave where fewer waves share a CU: 512 columns (96 VGPRs) for rows of at
+// least 4096 columns at 1024 threads, 1024 columns (162 VGPRs) for grids of
+// at most two 256-thread workgroups per CU.
+template <int BLOCK, int NT, int KCH>
 __global__ __launch_bounds__(NT) void softmax_block4_kernel(SoftmaxBlockParams p)
 {
     constexpr int kRows4PerBlock = kRowsPerWave4 * (NT / 64);
@@ -174,7 +180,7 @@ __global__ __launch_bounds__(NT) void softmax_block4_kernel(SoftmaxBlockParams p
     for (int i = threadIdx.x; i < kTabEntries; i += NT) tab[i] = p.tab[i];
     __syncthreads();
 
-    constexpr int kCh = BLOCK < 256 ? 256 : BLOCK;        // columns per row per step
+    constexpr int kCh = BLOCK < KCH ? KCH : BLOCK;        // columns per row per step
     constexpr int kG = kCh / 64;                          // fp32x4 groups per lane per step
     constexpr int kGPB = BLOCK / 64;                      // groups per block (>= 1)
     constexpr int kBPS = kCh / BLOCK;                     // blocks per step
@@ -274,15 +280,15 @@ __global__ __launch_bounds__(NT) void softmax_block4_kernel(SoftmaxBlockParams p
     }
 }
 
-template <int NT>
+template <int NT, int KCH>
 hipError_t launch_block4(const SoftmaxBlockParams& p, hipStream_t st)
 {
     constexpr int kRows4PerBlock = kRowsPerWave4 * (NT / 64);
     const dim3 grid4((unsigned)((p.rows + kRows4PerBlock - 1) / kRows4PerBlock));
     switch (p.block) {
-    case 64: hipLaunchKernelGGL((softmax_block4_kernel<64, NT>), grid4, dim3(NT), 0, st, p); break;
-    case 128: hipLaunchKernelGGL((softmax_block4_kernel<128, NT>), grid4, dim3(NT), 0, st, p); break;
-    default: hipLaunchKernelGGL((softmax_block4_kernel<256, NT>), grid4, dim3(NT), 0, st, p); break;
+    case 64: hipLaunchKernelGGL((softmax_block4_kernel<64, NT, KCH>), grid4, dim3(NT), 0, st, p); break;
+    case 128: hipLaunchKernelGGL((softmax_block4_kernel<128, NT, KCH>), grid4, dim3(NT), 0, st, p); break;
+    default: hipLaunchKernelGGL((softmax_block4_kernel<256, NT, KCH>), grid4, dim3(NT), 0, st, p); break;
     }
     return hipGetLastError();
 }
@@ -306,7 +312,11 @@ hipError_t launch_softmax_block(const SoftmaxBlockParams& p, hipStream_t st)
             if (dev >= 0 && dev < 64) ncu_of[dev].store(ncu, std::memory_order_relaxed);
         }
         const long long wg1024 = (p.rows + 4 * 16 - 1) / (4 * 16);
-        return wg1024 >= ncu ? launch_block4<1024>(p, st) : launch_block4<256>(p, st);
+        if (wg1024 >= ncu) return p.cols >= 4096 ? launch_block4<1024, 512>(p, st) : launch_block4<1024, 256>(p, st);
+        // fewer rows than CUs x 64: at most two 256-thread workgroups per CU
+        // take 1024 columns per step (162 VGPRs), more take 256
+        const long long wg256 = (p.rows + 4 * 4 - 1) / (4 * 4);
+        return wg256 <= 2 * ncu ? launch_block4<256, 1024>(p, st) : launch_block4<256, 256>(p, st);
     }
     const dim3 grid((unsigned)((p.rows + kRowsPerBlock - 1) / kRowsPerBlock));
     switch (p.block) {

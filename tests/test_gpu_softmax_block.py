@@ -109,3 +109,21 @@ def test_row_group_path_wide_launch(block):
     s = random_scores(16384 + 37, 4 * block + 4, seed=block + 11, std=6.0, masked_frac=0.02)
     s[-1, :] = -np.inf
     _compare(s, block)
+
+
+def test_row_group_path_wide_launch_long_rows():
+    # rows of at least 4096 columns at the 1024-thread launch: 512 columns per
+    # step, with a ragged last step and a ragged last workgroup
+    s = random_scores(16384 + 37, 4096 + 132, seed=23, std=6.0, masked_frac=0.02)
+    s[-1, :] = -np.inf
+    s[3, 4000:] += np.float32(9.0)              # a late maximum forces restarts
+    _compare(s, 128)
+
+
+@pytest.mark.parametrize("rows", [12288 + 5, 4096 + 3])
+def test_row_group_path_step_widths(rows):
+    # fewer rows than one 64-row workgroup per CU: more than two 256-thread
+    # workgroups per CU step 256 columns at a time, at most two step 1024
+    s = random_scores(rows, 2048 + 516, seed=rows, std=6.0, masked_frac=0.02)
+    s[1, :] = -np.inf
+    _compare(s, 128)
