@@ -1,0 +1,92 @@
+"""Seeded random shapes through the library's own dispatch (GPU): batch, head
+counts and grouping, query and key lengths (ragged against every tile and
+block size), head dimension, causal or not, block size, the Alg. 1 knobs and
+the input recipe are drawn per case, and every output row is judged by the
+two-stage parity check of helpers.check_parity.  A second set draws
+single-sequence and small-batch decode shapes that take the split-key path,
+which must also agree with the one-pass kernels."""
+import numpy as np
+import pytest
+
+from helpers import check_parity, dev_bf16
+from paper_2602_02071_amd.workloads import make_qkv
+
+pytestmark = pytest.mark.gpu
+
+N_CASES = 24
+N_SPLIT = 8
+MAX_SCORES = 6_000_000          # B * Hq * Sq * Sk per case: the oracle finishes in about a second
+
+
+def _draw(i):
+    g = np.random.Generator(np.random.PCG64(9000 + i))
+    while True:
+        D = int(g.choice([64, 128]))
+        block = int(g.choice([32, 64, 128]))
+        Hkv = int(g.choice([1, 2, 4]))
+        G = int(g.choice([1, 2, 4, 8]))
+        B = int(g.integers(1, 4))
+        decode_like = g.random() < 0.3
+        Sq = int(g.integers(1, 17)) if decode_like else int(g.integers(1, 700))
+        Sk = int(g.integers(1, 2500))
+        causal = bool(g.random() < 0.5)
+        if B * Hkv * G * Sq * Sk <= MAX_SCORES:
+            break
+    knobs = {}
+    if g.random() < 0.3:
+        knobs = dict(lam=int(g.choice([-1, 0, 2, 5])), n_b0=int(g.choice([0, 1, 2])))
+    recipe = dict(outliers=bool(g.random() < 0.5), lognormal_k=bool(g.random() < 0.3),
+                  sink=int(g.choice([0, 0, 4])))
+    return (B, Hkv * G, Hkv, Sq, Sk, D, causal), block, knobs, recipe
+
+
+def _run(q, k, v, shape, block, split=False, **knobs):
+    import torch
+    import paper_2602_02071_amd as baps
+    B, Hq, Hkv, Sq, Sk, D, causal = shape
+    o, lse = baps.attention(dev_bf16(q), dev_bf16(k), dev_bf16(v), causal, block, split=split, **knobs)
+    torch.cuda.synchronize()
+    return o.cpu().numpy().reshape(-1, D).astype(np.float64), lse.cpu().numpy().reshape(-1).astype(np.float64)
+
+
+@pytest.mark.parametrize("i", range(N_CASES))
+def test_random_shape(i):
+    shape, block, knobs, recipe = _draw(i)
+    label = f"case {i}: shape {shape} block {block} knobs {knobs} inputs {recipe}"
+    print(label, flush=True)
+    q, k, v = make_qkv(*shape[:6], seed=700 + i, **recipe)
+    o, lse = _run(q, k, v, shape, block, **knobs)
+    check_parity(q, k, v, shape, block, o, lse, label=label, **knobs)
+
+
+def _draw_split(i):
+    import paper_2602_02071_amd as baps
+    g = np.random.Generator(np.random.PCG64(9500 + i))
+    while True:
+        D = int(g.choice([64, 128]))
+        block = int(g.choice([32, 64, 128]))
+        Hkv = int(g.choice([1, 2, 4, 8]))
+        G = int(g.choice([1, 2, 4, 8]))
+        B = int(g.integers(1, 3))
+        Sq = int(g.integers(1, max(2, 64 // G) + 1))
+        Sk = int(g.integers(4 * block, 24000))
+        causal = bool(g.random() < 0.5)
+        shape = (B, Hkv * G, Hkv, Sq, Sk, D, causal)
+        if (B * Hkv * G * Sq * Sk <= MAX_SCORES
+                and baps.baps_attention_split_workspace(B, Hkv * G, Hkv, Sq, Sk, D, block) > 0):
+            return shape, block
+
+
+@pytest.mark.parametrize("i", range(N_SPLIT))
+def test_random_split_shape(i):
+    shape, block = _draw_split(i)
+    label = f"split case {i}: shape {shape} block {block}"
+    print(label, flush=True)
+    q, k, v = make_qkv(*shape[:6], seed=800 + i, outliers=True, lognormal_k=bool(i % 2))
+    o, lse = _run(q, k, v, shape, block, split=True)
+    o1, lse1 = _run(q, k, v, shape, block)
+    fin = np.isfinite(lse1)
+    assert np.array_equal(fin, np.isfinite(lse))
+    assert np.abs(o - o1).max() <= 2e-5 * max(1.0, np.abs(o1).max())
+    assert np.abs(lse[fin] - lse1[fin]).max() <= 1e-5
+    check_parity(q, k, v, shape, block, o, lse, label=label, same_kernels=False)
