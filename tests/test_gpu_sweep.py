@@ -4,10 +4,14 @@ block size), head dimension, causal or not, block size, the Alg. 1 knobs and
 the input recipe are drawn per case, and every output row is judged by the
 two-stage parity check of helpers.check_parity.  A second set draws
 single-sequence and small-batch decode shapes that take the split-key path,
-which must also agree with the one-pass kernels."""
+which must also agree with the one-pass kernels.  A third set draws one
+setup per case on top of a random shape: the Default and Exp2 HiF8 softmax
+setups, ties to even, tile-level restart, the diagonal B0 block, FP8 Q/K
+(inputs without outlier channels) and bf16 O."""
 import numpy as np
 import pytest
 
+import oracle as O
 from helpers import check_parity, dev_bf16
 from paper_2602_02071_amd.workloads import make_qkv
 
@@ -90,3 +94,65 @@ def test_random_split_shape(i):
     assert np.abs(o - o1).max() <= 2e-5 * max(1.0, np.abs(o1).max())
     assert np.abs(lse[fin] - lse1[fin]).max() <= 1e-5
     check_parity(q, k, v, shape, block, o, lse, label=label, same_kernels=False)
+
+
+N_SETUP = 24
+SETUPS = ("default", "exp2_hif8", "ties_even", "tiles", "b0_last", "fp8", "fp8_default", "out_bf16")
+
+
+def _draw_setup(i):
+    g = np.random.Generator(np.random.PCG64(9800 + i))
+    setup = SETUPS[i % len(SETUPS)]
+    shape, block, knobs, recipe = _draw(1000 + i)
+    B, Hq, Hkv, Sq, Sk, D, causal = shape
+    G = Hq // Hkv
+    if setup in ("ties_even", "fp8", "fp8_default") or "lam" in knobs and knobs["lam"] > 8:
+        knobs = {}
+    if setup == "tiles":
+        R = int(g.choice([r for r in (2, 4, 8, 16, 32, 64) if r * G <= 256]))
+        knobs = dict(knobs, restart_rows=R, b0_last=bool(g.random() < 0.5))
+    elif setup == "b0_last":
+        knobs = dict(knobs, b0_last=True)
+    if setup.startswith("fp8"):
+        recipe = dict(recipe, outliers=False)
+    return setup, shape, block, knobs, recipe
+
+
+@pytest.mark.parametrize("i", range(N_SETUP))
+def test_random_setup(i):
+    import torch
+    import paper_2602_02071_amd as baps
+    from paper_2602_02071_amd.workloads import make_qk_fp8
+    setup, shape, block, knobs, recipe = _draw_setup(i)
+    B, Hq, Hkv, Sq, Sk, D, causal = shape
+    label = f"setup case {i}: {setup} shape {shape} block {block} knobs {knobs} inputs {recipe}"
+    print(label, flush=True)
+    q, k, v = make_qkv(*shape[:6], seed=900 + i, **recipe)
+    mode = {"default": O.DEFAULT, "exp2_hif8": O.EXP2_HIF8, "fp8_default": O.DEFAULT}.get(setup, O.E2E_HIF8)
+    gkw = dict(knobs, mode=mode)
+    okw = dict(knobs, mode=mode, pv_bf16=(mode == O.DEFAULT))
+    if setup == "ties_even":
+        gkw["tie_mode"] = baps.BAPS_TIES_EVEN
+        okw["tie_even"] = True
+    fp8 = None
+    if setup.startswith("fp8"):
+        q8, k8, qs, ks = make_qk_fp8(q, k)
+        fp8 = (q8, k8, qs, ks)
+        qt = torch.from_numpy(np.ascontiguousarray(q8)).to("cuda:0")
+        kt = torch.from_numpy(np.ascontiguousarray(k8)).to("cuda:0")
+        gkw["qk_scales"] = (qs, ks)
+        q, k = O.e4m3_to_bf16(q8), O.e4m3_to_bf16(k8)
+        okw["scale_log2"] = O.fp8_scale_log2(D, qs, ks)
+    else:
+        qt, kt = dev_bf16(q), dev_bf16(k)
+    o, lse = baps.attention(qt, kt, dev_bf16(v), causal, block, out_bf16=(setup == "out_bf16"), **gkw)
+    torch.cuda.synchronize()
+    if setup == "out_bf16":
+        o32, lse32 = baps.attention(qt, kt, dev_bf16(v), causal, block, **gkw)
+        torch.cuda.synchronize()
+        assert torch.equal(o.view(torch.int16), o32.to(torch.bfloat16).view(torch.int16))
+        assert torch.equal(lse, lse32)
+        o = o32
+    o = o.float().cpu().numpy().reshape(-1, D).astype(np.float64)
+    lse = lse.cpu().numpy().reshape(-1).astype(np.float64)
+    check_parity(q, k, v, shape, block, o, lse, label=label, fp8=fp8, **okw)
