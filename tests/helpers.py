@@ -117,6 +117,20 @@ def lse_arb_tol(lse_ref, n_keys):
     return ARB_LSE_TOL + np.asarray(n_keys) * 2.0 ** -23 + 2.0 * np.spacing(mag).astype(np.float64)
 
 
+def lse_agree(lse, lse_ref, tol=1e-5):
+    """lse of two kernel paths whose sums differ only in order: within tol
+    plus two fp32 ulps at the magnitude of lse (its last roundings happen
+    there).  -inf must match -inf."""
+    lse, lse_ref = np.asarray(lse, np.float64), np.asarray(lse_ref, np.float64)
+    fin = np.isfinite(lse_ref)
+    if not np.array_equal(fin, np.isfinite(lse)):
+        return False
+    if not fin.any():
+        return True
+    bound = tol + 2.0 * np.spacing(np.abs(lse_ref[fin]).astype(np.float32)).astype(np.float64)
+    return bool(np.all(np.abs(lse[fin] - lse_ref[fin]) <= bound))
+
+
 def errors(o, ref):
     rel = float(np.linalg.norm(o - ref) / max(np.linalg.norm(ref), 1e-300))
     mx = float(np.abs(o - ref).max()) if o.size else 0.0
