@@ -7,7 +7,8 @@ single-sequence and small-batch decode shapes that take the split-key path,
 which must also agree with the one-pass kernels.  A third set draws one
 setup per case on top of a random shape: the Default and Exp2 HiF8 softmax
 setups, ties to even, tile-level restart, the diagonal B0 block, FP8 Q/K
-(inputs without outlier channels) and bf16 O."""
+(inputs without outlier channels) and bf16 O.  A fourth set draws group
+sizes (query heads per key/value head) of 3 to 32, most not powers of two."""
 import numpy as np
 import pytest
 
@@ -156,3 +157,33 @@ def test_random_setup(i):
     o = o.float().cpu().numpy().reshape(-1, D).astype(np.float64)
     lse = lse.cpu().numpy().reshape(-1).astype(np.float64)
     check_parity(q, k, v, shape, block, o, lse, label=label, fp8=fp8, **okw)
+
+
+N_GROUP = 12
+
+
+def _draw_group(i):
+    g = np.random.Generator(np.random.PCG64(9900 + i))
+    while True:
+        G = int(g.choice([3, 5, 6, 7, 12, 16, 32]))
+        Hkv = int(g.choice([1, 2, 3]))
+        B = int(g.integers(1, 3))
+        Sq = int(g.choice([1, 2, 3, int(g.integers(4, 65)), int(g.integers(65, 400))]))
+        Sk = int(g.integers(1, 3000))
+        D = int(g.choice([64, 128]))
+        block = int(g.choice([32, 64, 128]))
+        causal = bool(g.random() < 0.5)
+        if B * Hkv * G * Sq * Sk <= MAX_SCORES:
+            return (B, Hkv * G, Hkv, Sq, Sk, D, causal), block
+
+
+@pytest.mark.parametrize("i", range(N_GROUP))
+def test_random_group_size(i):
+    # query heads per key/value head that are not powers of two, and large
+    # groups whose rows fill a tile from few query positions
+    shape, block = _draw_group(i)
+    label = f"group case {i}: shape {shape} block {block}"
+    print(label, flush=True)
+    q, k, v = make_qkv(*shape[:6], seed=1000 + i, outliers=bool(i % 2), lognormal_k=bool(i % 3 == 0))
+    o, lse = _run(q, k, v, shape, block)
+    check_parity(q, k, v, shape, block, o, lse, label=label)
