@@ -56,7 +56,7 @@ DEFAULT_FLIP_TOL = 2e-3
 # the GPU tests append one JSON record per parity check here
 PARITY_LOG = os.environ.get("BAPS_PARITY_LOG",
                             os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
-                                         "gpurun_out", "parity_records.jsonl"))
+                                         "test_records", "parity_records.jsonl"))
 
 
 def dev_bf16(x):
