@@ -5,9 +5,9 @@
 // the Hq/Hkv query heads that share K/V share the item, and single-position
 // decode packs its heads into one tile.  Each wave owns 32 rows.  At D = 128
 // the grid is persistent: one workgroup per CU takes a sequence of items
-// (item_at), and the first K/V block of the next item loads during the last
-// block of the current one; at D = 64 a workgroup takes one item and two of
-// them share a CU.
+// (item_at); the first K/V block of the next item loads during the last
+// block of the current one, and its Q right after that block's Q^T reads;
+// at D = 64 a workgroup takes one item and two of them share a CU.
 //
 // Per key block j (the paper's key tile, visited in ascending order):
 //   - K_j and V_j arrive in LDS through asynchronous global->LDS loads into a
@@ -509,6 +509,7 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
         // state, 2^(ref_j - m_j) on the new block) fold into one exact rescale by
         // 2^(ref_{j-1} - ref_j), needed only when the reference moves, and the
         // normalisation O = O~/d = X/dX is unchanged.
+        bool q_ready = false;           // the next item's Q was loaded during the last block
         float m = ninf;                 // running integer maximum m_j
         float ref = ninf;               // current block reference
         float dl = 0.0f;                // this lane's share of dX
@@ -526,12 +527,13 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
             // the next block of this item, or the first block of the next
             // item while the last one is computed
             const bool last = jb + 1 == cur.nblk;
+            ItemGeo e_next;
+            bool has_next = false;
             if (!last) {
                 issue_block(hoff_cur, jb + 1, sel ^ 1);
             } else if constexpr (PERSIST) {
-                ItemGeo e;
-                if (item_of_round<BLK, C::kTileRows>(fresh_args(), rnd + 1, e) && e.nblk > 0)
-                    issue_block(kv_off(e), 0, sel ^ 1);
+                has_next = item_of_round<BLK, C::kTileRows>(fresh_args(), rnd + 1, e_next);
+                if (has_next && e_next.nblk > 0) issue_block(kv_off(e_next), 0, sel ^ 1);
             }
             // A wave that sees nothing of the block skips it.  In a tile that
             // spans waves it still takes part in the tile's exchange below, with
@@ -590,6 +592,14 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
             }
             __builtin_amdgcn_sched_barrier(0);
             __builtin_amdgcn_s_setprio(0);
+            if constexpr (PERSIST) {
+                // the last block's Q^T reads are done: the next item's Q loads
+                // behind this block's softmax and PV
+                if (has_next) {
+                    load_q(fresh_args(), e_next);
+                    q_ready = true;
+                }
+            }
             // mask keys past kmax (causal diagonal, ragged tail); key of register
             // i of tile kt: key0 + 32*kt + 8*(i/4) + 4*half + i%4
             if (key0 + BLK - 1 > kmax_wave_lo) {
@@ -860,7 +870,7 @@ __global__ __launch_bounds__(64 * NW) void baps_attn_fwd_kernel(AttnParams p)
         ItemGeo nxt;
         if (!PERSIST || !item_of_round<BLK, C::kTileRows>(a, rnd + 1, nxt)) break;
         if (cur.nblk == 0 && nxt.nblk > 0) issue_block(kv_off(nxt), 0, sel);
-        load_q(a, nxt);
+        if (!q_ready) load_q(a, nxt);
         cur = nxt;
     }
 }
