@@ -64,6 +64,13 @@ def test_prefill_fp8(case):
     _run(shape, block, seed=sum(shape))
 
 
+def test_prefill_fp8_several_items_per_workgroup():
+    # 288 work items of 256 rows at D = 128: more than the GPU holds at once,
+    # so the persistent workgroups take a second item, whose FP8 Q loads
+    # during the last key block of the first
+    _run((1, 32, 8, 2304, 512, 128, True), 128, seed=77)
+
+
 DECODE = [
     ((3, 8, 2, 1, 777, 64, False), 64),        # D 64: half of the 16x16x128 contraction is zero
     ((2, 8, 1, 1, 1030, 128, False), 128),
